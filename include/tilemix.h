@@ -1,0 +1,167 @@
+/*
+ * tilemix.h -- C ABI of the MI355X (gfx950) TileMix routed prefill attention library.
+ *
+ * What the library computes (TileMix, arXiv 2608.17336):
+ *   Causal (or full) softmax attention O = softmax(S) V over dense FP16 tensors
+ *   (Section 3.1), where every legal score tile of BLOCK_M query rows by
+ *   BLOCK_N keys is produced by one of two paths chosen by a packed routing
+ *   bit (Sections 4.2 and 4.3):
+ *     bit 0 (FP16):  S = scale * Q K^T with FP16 operands and FP32 accumulation;
+ *     bit 1 (INT8):  S = scale * dQ * dK * (Q8 K8^T), Q8/K8 the blockwise
+ *                    symmetric INT8 codes of Q and K with one FP16 scale per
+ *                    128-token query block / 64-token key block and head,
+ *                    the product accumulated exactly in INT32 (Appendix C).
+ *   Both paths feed one online-softmax state; V and the P.V product stay FP16
+ *   (Appendix C, "INT8 Score Computation" and "Quantize-Once Execution").
+ *
+ * Conventions shared by every entry point:
+ *   - Tensors are dense and contiguous, token-major with interleaved heads:
+ *       Q, O : FP16 [B, L_q, H_q, d]      K, V : FP16 [B, L_k, H_k, d]
+ *     Query head h_q reads KV head h_k = h_q / (H_q / H_k) (Section 4.1).
+ *   - Routing words: uint64 [B_r, H_k, T_m, W] with T_m = ceil(L_q / BLOCK_M),
+ *     T_n = ceil(L_k / BLOCK_N), T_mask = ceil(T_n / g) routing groups per row
+ *     and W = ceil(T_mask / 64) words per row.  Key tile n belongs to group
+ *     g_j = n / g, found in word g_j / 64 at bit g_j % 64; 1 = INT8, 0 = FP16
+ *     (Section 4.2, "Bitmask packing" and "Constant-time lookup").  With
+ *     W == 1 this is the paper's one-word-per-row layout; longer rows continue
+ *     into further words.  B_r is 1 (one map for every sequence, as in the
+ *     paper) unless params.route_per_batch is 1, then B_r = B.
+ *     Bits of groups that hold no legal (query, key) pair, and bits at
+ *     positions >= T_mask, are ignored.
+ *   - Legality (causal and sequence-boundary masks) is decided in the kernel,
+ *     independently of routing (Section 4.1).  With causal = 1 key j is legal
+ *     for query i iff j <= i + (L_k - L_q) (bottom-right alignment); a query
+ *     row with no legal key produces zeros.
+ *   - Pointers named "device" must be device memory (hipMalloc / torch CUDA
+ *     tensors) on the current device; the caller owns every buffer.  The
+ *     library allocates nothing, never synchronizes, and keeps no state
+ *     between calls, so calls on different streams with distinct outputs and
+ *     workspaces may run concurrently.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     All device work is enqueued on it; the call returns without waiting.
+ *   - Errors: argument problems are detected before anything is enqueued and
+ *     returned as a status (tilemix_last_error() gives a message, per thread).
+ *     A failed kernel launch returns TILEMIX_ERR_HIP.  Faults during execution
+ *     surface at the caller's next synchronization, as usual for HIP.
+ */
+#ifndef TILEMIX_H
+#define TILEMIX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum tilemix_status {
+  TILEMIX_OK = 0,
+  TILEMIX_ERR_NULL = 1,         /* a required pointer is NULL */
+  TILEMIX_ERR_SHAPE = 2,        /* sizes inconsistent or out of range */
+  TILEMIX_ERR_UNSUPPORTED = 3,  /* d, tile shape or flags this build does not implement */
+  TILEMIX_ERR_ALIGN = 4,        /* a pointer is not aligned as required */
+  TILEMIX_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than tilemix_workspace_size() */
+  TILEMIX_ERR_HIP = 6           /* the HIP runtime rejected a launch */
+} tilemix_status;
+
+/* Problem description shared by all entry points. */
+typedef struct tilemix_params {
+  int32_t batch;          /* B >= 1 */
+  int32_t heads_q;        /* H_q >= 1 */
+  int32_t heads_kv;       /* H_k >= 1 and H_q % H_k == 0 */
+  int32_t len_q;          /* L_q >= 1 */
+  int32_t len_k;          /* L_k >= 1 */
+  int32_t head_dim;       /* d: 64 or 128 */
+  int32_t block_m;        /* BLOCK_M (query rows per routed tile): 64 or 128 */
+  int32_t block_n;        /* BLOCK_N (keys per routed tile): 64 */
+  int32_t group_size;     /* g >= 1: one routing bit per g adjacent key tiles */
+  int32_t causal;         /* 0 or 1 */
+  float scale;            /* softmax scale (1/sqrt(d) for standard attention); finite, > 0 */
+  int32_t route_per_batch;/* 0: routing words shared by the batch (B_r = 1); 1: B_r = B */
+  int32_t route_hint;     /* -1: unknown; 0: the map has no INT8 bit (quantization is skipped
+                             and every tile takes the FP16 path); other values: invalid */
+} tilemix_params;
+
+/* Words per routing row, W = ceil(ceil(ceil(L_k / BLOCK_N) / g) / 64); 0 if params invalid. */
+int32_t tilemix_route_words_per_row(const tilemix_params* params);
+
+/* Bytes of device workspace tilemix_prefill needs (Q8, K8, their FP16 block scales and
+ * V laid out per 64-key tile); the workspace must be 256-byte aligned. */
+tilemix_status tilemix_workspace_size(const tilemix_params* params, size_t* bytes);
+
+/*
+ * tilemix_prefill -- routed attention forward: O = Attention(Q, K, V) with per-tile-group
+ * FP16/INT8 score routing (Sections 3.1, 4.1-4.3, Appendix C).
+ *   Q          device FP16 [B, L_q, H_q, d], 16-byte aligned, read only
+ *   K, V       device FP16 [B, L_k, H_k, d], 16-byte aligned, read only
+ *   route_bits device uint64 [B_r, H_k, T_m, W], 8-byte aligned, read only
+ *   O          device FP16 [B, L_q, H_q, d], 16-byte aligned, written (every element)
+ *   workspace  device scratch of at least tilemix_workspace_size() bytes, 256-byte aligned;
+ *              overwritten; must not be shared with a concurrently running call
+ * Enqueues the operand preparation (skipped parts: see route_hint) and the fused kernel.
+ */
+tilemix_status tilemix_prefill(const tilemix_params* params,
+                               const void* Q, const void* K, const void* V,
+                               const uint64_t* route_bits, void* O,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * tilemix_prepare -- the first half of tilemix_prefill: the quantize-once pass (Q8, K8 and
+ * their FP16 block scales, Appendix C "Quantize-Once Execution"; skipped when route_hint is 0)
+ * and the per-64-key-tile V layout, written into `workspace`.  Arguments as in
+ * tilemix_prefill.  The workspace then serves any number of tilemix_attend calls on the same
+ * Q, K and V.
+ */
+tilemix_status tilemix_prepare(const tilemix_params* params, const void* Q, const void* K,
+                               const void* V, void* workspace, size_t workspace_bytes,
+                               void* stream);
+
+/*
+ * tilemix_attend -- the second half of tilemix_prefill: the fused routed attention kernel
+ * (Sections 3.1, 4.2, 4.3) reading Q, K and the prepared workspace.  `params`, Q and K must
+ * be those of the tilemix_prepare call that filled the workspace (route_hint included);
+ * route_bits may differ between calls.  Arguments as in tilemix_prefill.
+ */
+tilemix_status tilemix_attend(const tilemix_params* params, const void* Q, const void* K,
+                              const uint64_t* route_bits, void* O, const void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/*
+ * tilemix_quantize -- the quantize-once operand preparation on its own (Appendix C,
+ * "Blockwise INT8 Quantization", "Quantization Granularity", "Quantize-Once Execution").
+ *   Q, K  device FP16 as in tilemix_prefill
+ *   Q8    device int8 [B, L_q, H_q, d] written;  dQ device FP16 bits [B, ceil(L_q/128), H_q]
+ *   K8    device int8 [B, L_k, H_k, d] written;  dK device FP16 bits [B, ceil(L_k/64), H_k]
+ * Scale = block absmax / 127 in FP32 (IEEE division), code = round-half-even(x / scale)
+ * clamped to [-127, 127], a zero block gets codes 0 and scale 0, the scale is stored as FP16
+ * (round to nearest even).  Q8/K8 16-byte aligned, dQ/dK 2-byte aligned.
+ */
+tilemix_status tilemix_quantize(const tilemix_params* params, const void* Q, const void* K,
+                                int8_t* Q8, uint16_t* dQ, int8_t* K8, uint16_t* dK, void* stream);
+
+/*
+ * tilemix_debug_qk_int32 -- the INT32 tile products C = Q8_m K8_n^T of the INT8 score path
+ * (Appendix C, "INT8 Score Computation"), computed with the same MFMA code as the fused
+ * kernel, for checking bit-exactness.
+ *   Q8, K8  device int8 as written by tilemix_quantize
+ *   tiles   device int32 [count, 4] rows (b, h_q, m, n): query tile m, key tile n
+ *   out     device int32 [count, BLOCK_M, BLOCK_N] row-major (query row, key column);
+ *           entries past L_q or L_k are 0
+ * A tile row whose (b, h_q, m, n) lies out of range yields an all-zero tile; count < 0 is an
+ * error and count == 0 enqueues nothing.
+ */
+tilemix_status tilemix_debug_qk_int32(const tilemix_params* params, const int8_t* Q8,
+                                      const int8_t* K8, const int32_t* tiles, int32_t count,
+                                      int32_t* out, void* stream);
+
+/* Static description of a status code. */
+const char* tilemix_status_string(tilemix_status status);
+
+/* Message describing the last error returned on the calling thread ("" if none). */
+const char* tilemix_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TILEMIX_H */

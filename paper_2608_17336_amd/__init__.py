@@ -1,0 +1,300 @@
+"""Python binding of libtilemix.so (TileMix routed prefill attention for MI355X / gfx950).
+
+Argument marshalling only: every step of the attention path runs in the HIP kernels of
+libtilemix.so.  PyTorch provides device memory and streams.  The functions carry the names
+of the C entry points declared in include/tilemix.h.  Importing this module does not load
+the library; the first call does, and raises if it has not been built
+(``python paper_2608_17336_amd/build.py`` or ``__graft_entry__.build()``).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+__all__ = [
+    "TilemixError",
+    "Params",
+    "library_path",
+    "load_library",
+    "tilemix_route_words_per_row",
+    "tilemix_workspace_size",
+    "tilemix_prefill",
+    "tilemix_prepare",
+    "tilemix_attend",
+    "tilemix_quantize",
+    "tilemix_debug_qk_int32",
+    "EXPORTED_SYMBOLS",
+]
+
+EXPORTED_SYMBOLS = (
+    "tilemix_route_words_per_row",
+    "tilemix_workspace_size",
+    "tilemix_prefill",
+    "tilemix_prepare",
+    "tilemix_attend",
+    "tilemix_quantize",
+    "tilemix_debug_qk_int32",
+    "tilemix_status_string",
+    "tilemix_last_error",
+)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, "libtilemix.so")
+
+
+class TilemixError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"tilemix status {status}: {message}")
+        self.status = status
+
+
+class _CParams(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("heads_q", ctypes.c_int32),
+        ("heads_kv", ctypes.c_int32),
+        ("len_q", ctypes.c_int32),
+        ("len_k", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_m", ctypes.c_int32),
+        ("block_n", ctypes.c_int32),
+        ("group_size", ctypes.c_int32),
+        ("causal", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+        ("route_per_batch", ctypes.c_int32),
+        ("route_hint", ctypes.c_int32),
+    ]
+
+
+@dataclass(frozen=True)
+class Params:
+    """Mirror of ``tilemix_params``."""
+    batch: int
+    heads_q: int
+    heads_kv: int
+    len_q: int
+    len_k: int
+    head_dim: int
+    block_m: int = 128
+    block_n: int = 64
+    group_size: int = 1
+    causal: bool = True
+    scale: float = 0.0          # 0 -> 1/sqrt(head_dim)
+    route_per_batch: bool = False
+    route_hint: int = -1
+
+    def c(self) -> _CParams:
+        scale = self.scale if self.scale else 1.0 / math.sqrt(self.head_dim)
+        return _CParams(self.batch, self.heads_q, self.heads_kv, self.len_q, self.len_k,
+                        self.head_dim, self.block_m, self.block_n, self.group_size,
+                        int(bool(self.causal)), scale, int(bool(self.route_per_batch)),
+                        self.route_hint)
+
+    @property
+    def T_m(self) -> int:
+        return -(-self.len_q // self.block_m)
+
+    @property
+    def T_n(self) -> int:
+        return -(-self.len_k // self.block_n)
+
+
+_LIB = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Load libtilemix.so (raises if it is missing: there is no fallback path)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER(_CParams)
+    vp = ctypes.c_void_p
+    lib.tilemix_route_words_per_row.argtypes = [P]
+    lib.tilemix_route_words_per_row.restype = ctypes.c_int32
+    lib.tilemix_workspace_size.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+    lib.tilemix_workspace_size.restype = ctypes.c_int
+    lib.tilemix_prefill.argtypes = [P, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.tilemix_prefill.restype = ctypes.c_int
+    lib.tilemix_prepare.argtypes = [P, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.tilemix_prepare.restype = ctypes.c_int
+    lib.tilemix_attend.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.tilemix_attend.restype = ctypes.c_int
+    lib.tilemix_quantize.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
+    lib.tilemix_quantize.restype = ctypes.c_int
+    lib.tilemix_debug_qk_int32.argtypes = [P, vp, vp, vp, ctypes.c_int32, vp, vp]
+    lib.tilemix_debug_qk_int32.restype = ctypes.c_int
+    lib.tilemix_status_string.argtypes = [ctypes.c_int]
+    lib.tilemix_status_string.restype = ctypes.c_char_p
+    lib.tilemix_last_error.argtypes = []
+    lib.tilemix_last_error.restype = ctypes.c_char_p
+    _LIB = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        lib = load_library()
+        msg = lib.tilemix_last_error().decode() or lib.tilemix_status_string(status).decode()
+        raise TilemixError(status, msg)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def tilemix_route_words_per_row(params: Params) -> int:
+    return int(load_library().tilemix_route_words_per_row(ctypes.byref(params.c())))
+
+
+def tilemix_workspace_size(params: Params) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().tilemix_workspace_size(ctypes.byref(params.c()), ctypes.byref(n)))
+    return int(n.value)
+
+
+def _require(t, dtype, shape, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint) -> Params:
+    B, Lq, Hq, d = Q.shape
+    Lk, Hk = K.shape[1], K.shape[2]
+    return Params(B, Hq, Hk, Lq, Lk, d, tile[0], tile[1], group_size, causal,
+                  scale if scale else 1.0 / math.sqrt(d), route_per_batch, route_hint)
+
+
+def _check_inputs(p: Params, Q, K, V=None):
+    import torch
+    _require(Q, torch.float16, (p.batch, p.len_q, p.heads_q, p.head_dim), "Q")
+    _require(K, torch.float16, (p.batch, p.len_k, p.heads_kv, p.head_dim), "K")
+    if V is not None:
+        _require(V, torch.float16, (p.batch, p.len_k, p.heads_kv, p.head_dim), "V")
+
+
+def _workspace(p: Params, workspace, device):
+    import torch
+    need = tilemix_workspace_size(p)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    nbytes = workspace.numel() * workspace.element_size()
+    if nbytes < need:
+        raise ValueError(f"workspace too small: {need} bytes needed")
+    return workspace, nbytes
+
+
+def _route_and_out(p: Params, Q, route_bits, O):
+    import torch
+    W = tilemix_route_words_per_row(p)
+    _require(route_bits, torch.int64, (p.batch if p.route_per_batch else 1, p.heads_kv, p.T_m, W),
+             "route_bits")
+    if O is None:
+        O = torch.empty((p.batch, p.len_q, p.heads_q, p.head_dim), dtype=torch.float16, device=Q.device)
+    _require(O, torch.float16, (p.batch, p.len_q, p.heads_q, p.head_dim), "O")
+    return O
+
+
+def tilemix_prefill(Q, K, V, route_bits, group_size: int, tile=(128, 64), causal: bool = True,
+                    scale: float | None = None, *, O=None, workspace=None, stream=None,
+                    route_per_batch: bool = False, route_hint: int = -1):
+    """Routed prefill attention.  Q [B, Lq, Hq, d], K/V [B, Lk, Hk, d] fp16 CUDA tensors,
+    route_bits uint64 words [B_r, Hk, T_m, W] as an int64 CUDA tensor (same bits).
+    Returns O (fp16, [B, Lq, Hq, d]).  ``workspace`` (uint8, >= tilemix_workspace_size)
+    is allocated when not given."""
+    p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
+    _check_inputs(p, Q, K, V)
+    O = _route_and_out(p, Q, route_bits, O)
+    workspace, nbytes = _workspace(p, workspace, Q.device)
+    cp = p.c()
+    _check(load_library().tilemix_prefill(
+        ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace),
+        ctypes.c_size_t(nbytes), _stream(stream)))
+    return O
+
+
+def tilemix_prepare(Q, K, V, group_size: int, tile=(128, 64), causal: bool = True,
+                    scale: float | None = None, *, workspace=None, stream=None,
+                    route_per_batch: bool = False, route_hint: int = -1):
+    """Operand preparation (quantize-once + V tile layout) into ``workspace``; returns it."""
+    p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
+    _check_inputs(p, Q, K, V)
+    workspace, nbytes = _workspace(p, workspace, Q.device)
+    cp = p.c()
+    _check(load_library().tilemix_prepare(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(workspace),
+                                          ctypes.c_size_t(nbytes), _stream(stream)))
+    return workspace
+
+
+def tilemix_attend(Q, K, route_bits, workspace, group_size: int, tile=(128, 64), causal: bool = True,
+                   scale: float | None = None, *, O=None, stream=None, route_per_batch: bool = False,
+                   route_hint: int = -1):
+    """Fused routed attention on a workspace filled by tilemix_prepare; returns O."""
+    p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
+    _check_inputs(p, Q, K)
+    O = _route_and_out(p, Q, route_bits, O)
+    workspace, nbytes = _workspace(p, workspace, Q.device)
+    cp = p.c()
+    _check(load_library().tilemix_attend(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(route_bits), _ptr(O),
+                                         _ptr(workspace), ctypes.c_size_t(nbytes), _stream(stream)))
+    return O
+
+
+def tilemix_quantize(Q, K, *, tile=(128, 64), stream=None):
+    """Quantize-once pass.  Returns (Q8 int8, dQ fp16, K8 int8, dK fp16) CUDA tensors."""
+    import torch
+    B, Lq, Hq, d = Q.shape
+    Lk, Hk = K.shape[1], K.shape[2]
+    p = Params(B, Hq, Hk, Lq, Lk, d, tile[0], tile[1])
+    _require(Q, torch.float16, (B, Lq, Hq, d), "Q")
+    _require(K, torch.float16, (B, Lk, Hk, d), "K")
+    Q8 = torch.empty((B, Lq, Hq, d), dtype=torch.int8, device=Q.device)
+    K8 = torch.empty((B, Lk, Hk, d), dtype=torch.int8, device=Q.device)
+    dQ = torch.empty((B, -(-Lq // 128), Hq), dtype=torch.float16, device=Q.device)
+    dK = torch.empty((B, -(-Lk // 64), Hk), dtype=torch.float16, device=Q.device)
+    cp = p.c()
+    _check(load_library().tilemix_quantize(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(Q8), _ptr(dQ),
+                                           _ptr(K8), _ptr(dK), _stream(stream)))
+    return Q8, dQ, K8, dK
+
+
+def tilemix_debug_qk_int32(Q8, K8, tiles, *, heads_q: int, heads_kv: int, tile=(128, 64),
+                           stream=None):
+    """INT32 tile products for rows (b, h_q, m, n) of ``tiles`` (int32 CUDA [count, 4]).
+    Returns int32 [count, BLOCK_M, BLOCK_N]."""
+    import torch
+    B, Lq, Hq, d = Q8.shape
+    Lk = K8.shape[1]
+    p = Params(B, heads_q, heads_kv, Lq, Lk, d, tile[0], tile[1])
+    _require(Q8, torch.int8, (B, Lq, heads_q, d), "Q8")
+    _require(K8, torch.int8, (B, Lk, heads_kv, d), "K8")
+    count = tiles.shape[0]
+    _require(tiles, torch.int32, (count, 4), "tiles")
+    out = torch.empty((count, tile[0], tile[1]), dtype=torch.int32, device=Q8.device)
+    cp = p.c()
+    _check(load_library().tilemix_debug_qk_int32(ctypes.byref(cp), _ptr(Q8), _ptr(K8), _ptr(tiles),
+                                                 ctypes.c_int32(count), _ptr(out), _stream(stream)))
+    return out

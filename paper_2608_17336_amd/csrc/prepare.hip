@@ -1,0 +1,159 @@
+// prepare.hip -- operand preparation for the routed attention kernel (bandwidth-bound).
+//
+// quantize_blocks_kernel: the quantize-once pass of Appendix C ("Blockwise INT8
+//   Quantization", "Quantization Granularity", "Quantize-Once Execution"): for every
+//   (sequence, head, block of 128 query / 64 key tokens) the FP32 absmax, the FP32
+//   scale absmax/127, the codes round-half-even(x / scale) clamped to [-127, 127]
+//   and the FP16 scale.  One workgroup per block; the block is read once into
+//   registers, reduced, then converted and written.
+//
+// v_tiles_kernel: lays V out per 64-key tile as [d][64] so that the P.V matrix-core
+//   step reads its A operand (V^T) as contiguous 16-byte runs.  Within each run of
+//   16 keys the order is (0-3, 8-11 | 4-7, 12-15): this is the key order in which
+//   the score accumulator hands P to the P.V step (accumulator rows 8*(r/4) +
+//   4*(lane/32) + r%4), so P never leaves registers.  Keys past L are zero.
+#include "tilemix_device.h"
+#include "tilemix_internal.h"
+
+namespace tilemix {
+
+namespace {
+
+constexpr int kPrepThreads = 256;
+
+__device__ __forceinline__ float block_max(float v, float* red) {
+  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
+  const int wave = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) red[wave] = v;
+  __syncthreads();
+  float r = red[0];
+  for (int w = 1; w < kPrepThreads / kWave; ++w) r = fmaxf(r, red[w]);
+  return r;
+}
+
+template <int D, int BLK>
+__global__ __launch_bounds__(kPrepThreads) void quantize_blocks_kernel(
+    const _Float16* __restrict__ X, int8_t* __restrict__ X8, uint16_t* __restrict__ dX,
+    int L, int H, int nblk) {
+  constexpr int kChunksPerRow = D / 8;                          // 16-byte chunks of 8 halfs
+  constexpr int kPer = BLK * kChunksPerRow / kPrepThreads;      // chunks per thread
+  static_assert(kPer * kPrepThreads == BLK * kChunksPerRow, "block split");
+  __shared__ float red[kPrepThreads / kWave];
+
+  const int r = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int row0 = r * BLK;
+  const int rows = min(BLK, L - row0);
+
+  uint4 v[kPer];
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int c = threadIdx.x + kPrepThreads * i;
+    const int row = c / kChunksPerRow, ch = c % kChunksPerRow;
+    if (row < rows) {
+      const size_t off = (((size_t)b * L + row0 + row) * H + h) * D + ch * 8;
+      v[i] = ld_global_16(X + off);
+      const half8 hv = as_half8(v[i]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)hv[e]));
+    } else {
+      v[i] = make_uint4(0, 0, 0, 0);
+    }
+  }
+  amax = block_max(amax, red);
+  const float d32 = amax / 127.0f;   // IEEE FP32 division (no fast-math in this build)
+
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int c = threadIdx.x + kPrepThreads * i;
+    const int row = c / kChunksPerRow, ch = c % kChunksPerRow;
+    if (row < rows) {
+      const half8 hv = as_half8(v[i]);
+      uint32_t packed[2] = {0u, 0u};
+      if (amax > 0.0f) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float q = rintf((float)hv[e] / d32);          // round half to even
+          q = fminf(127.0f, fmaxf(-127.0f, q));
+          const uint32_t byte = (uint32_t)((int)q) & 0xffu;
+          packed[e >> 2] |= byte << (8 * (e & 3));
+        }
+      }
+      const size_t off = (((size_t)b * L + row0 + row) * H + h) * D + ch * 8;
+      *reinterpret_cast<uint2*>(X8 + off) = make_uint2(packed[0], packed[1]);
+    }
+  }
+  if (threadIdx.x == 0) {
+    const _Float16 s = (amax > 0.0f) ? (_Float16)d32 : (_Float16)0.0f;   // RNE
+    uint16_t bits;
+    __builtin_memcpy(&bits, &s, 2);
+    dX[((size_t)b * nblk + r) * H + h] = bits;
+  }
+}
+
+// Position p (0..63) of a V tile row holds key (16*(p/16) + 8*((p%8)/4) + 4*((p/8)%2) + p%4).
+__device__ __forceinline__ int vt_key_of_pos(int p) {
+  const int t = p >> 4, h = (p >> 3) & 1, e = p & 7;
+  return 16 * t + 8 * (e >> 2) + 4 * h + (e & 3);
+}
+
+template <int D>
+__global__ __launch_bounds__(kPrepThreads) void v_tiles_kernel(
+    const _Float16* __restrict__ V, _Float16* __restrict__ Vt, int L, int H, int T_n) {
+  constexpr int kRowHalfs = D + 8;                  // padded LDS row: 8 rows hit 8 bank groups
+  constexpr int kInChunks = kBlockN * D / 8;        // 16-byte chunks of the input tile
+  constexpr int kOutChunks = D * kBlockN / 8;
+  __shared__ __align__(16) _Float16 tile[kBlockN * kRowHalfs];
+
+  const int n = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int key0 = n * kBlockN;
+  for (int c = threadIdx.x; c < kInChunks; c += kPrepThreads) {
+    const int row = c / (D / 8), ch = c % (D / 8);
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (key0 + row < L) val = ld_global_16(V + (((size_t)b * L + key0 + row) * H + h) * D + ch * 8);
+    *reinterpret_cast<uint4*>(&tile[row * kRowHalfs + ch * 8]) = val;
+  }
+  __syncthreads();
+  _Float16* out = Vt + (((size_t)b * H + h) * T_n + n) * (size_t)(D * kBlockN);
+  for (int c = threadIdx.x; c < kOutChunks; c += kPrepThreads) {
+    const int d = c / 8, ch = c % 8;
+    half8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = tile[vt_key_of_pos(ch * 8 + e) * kRowHalfs + d];
+    *reinterpret_cast<half8*>(out + d * kBlockN + ch * 8) = o;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_quantize(const _Float16* X, int8_t* X8, uint16_t* dX, int B, int L, int H,
+                           int d, int block_rows, hipStream_t stream) {
+  const int nblk = (L + block_rows - 1) / block_rows;
+  dim3 grid(nblk, H, B), block(kPrepThreads);
+  if (d == 128 && block_rows == 128)
+    hipLaunchKernelGGL((quantize_blocks_kernel<128, 128>), grid, block, 0, stream, X, X8, dX, L, H, nblk);
+  else if (d == 128 && block_rows == 64)
+    hipLaunchKernelGGL((quantize_blocks_kernel<128, 64>), grid, block, 0, stream, X, X8, dX, L, H, nblk);
+  else if (d == 64 && block_rows == 128)
+    hipLaunchKernelGGL((quantize_blocks_kernel<64, 128>), grid, block, 0, stream, X, X8, dX, L, H, nblk);
+  else if (d == 64 && block_rows == 64)
+    hipLaunchKernelGGL((quantize_blocks_kernel<64, 64>), grid, block, 0, stream, X, X8, dX, L, H, nblk);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_v_tiles(const _Float16* V, _Float16* Vt, int B, int L, int H, int d,
+                          hipStream_t stream) {
+  const int T_n = (L + kBlockN - 1) / kBlockN;
+  dim3 grid(T_n, H, B), block(kPrepThreads);
+  if (d == 128)
+    hipLaunchKernelGGL((v_tiles_kernel<128>), grid, block, 0, stream, V, Vt, L, H, T_n);
+  else if (d == 64)
+    hipLaunchKernelGGL((v_tiles_kernel<64>), grid, block, 0, stream, V, Vt, L, H, T_n);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace tilemix

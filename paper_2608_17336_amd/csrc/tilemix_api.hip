@@ -1,0 +1,293 @@
+// tilemix_api.hip -- the C ABI declared in include/tilemix.h: argument validation, the
+// workspace plan and the launch sequence.  No allocation, no synchronization, no state
+// beyond a per-thread error message.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "tilemix.h"
+#include "tilemix_device.h"
+#include "tilemix_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+tilemix_status fail(tilemix_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+tilemix_status fail(tilemix_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+tilemix_status ok() {
+  g_last_error[0] = '\0';
+  return TILEMIX_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
+
+// Derived sizes of one problem.
+struct Plan {
+  long long T_m, T_n, T_mask, W;
+  long long nQB, nKB;
+  size_t q8_bytes, k8_bytes, dq_bytes, dk_bytes, vt_bytes;
+  size_t q8_off, k8_off, dq_off, dk_off, vt_off, total;
+};
+
+tilemix_status validate(const tilemix_params* p) {
+  if (!p) return fail(TILEMIX_ERR_NULL, "params is NULL");
+  if (p->batch < 1 || p->heads_q < 1 || p->heads_kv < 1 || p->len_q < 1 || p->len_k < 1)
+    return fail(TILEMIX_ERR_SHAPE, "batch, heads and lengths must be >= 1");
+  if (p->heads_q % p->heads_kv != 0)
+    return fail(TILEMIX_ERR_SHAPE, "heads_q (%d) must be a multiple of heads_kv (%d)", p->heads_q,
+                p->heads_kv);
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(TILEMIX_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", p->head_dim);
+  if (p->block_m != 64 && p->block_m != 128)
+    return fail(TILEMIX_ERR_UNSUPPORTED, "block_m %d not supported (64 or 128)", p->block_m);
+  if (p->block_n != 64)
+    return fail(TILEMIX_ERR_UNSUPPORTED, "block_n %d not supported (64)", p->block_n);
+  if (p->group_size < 1) return fail(TILEMIX_ERR_SHAPE, "group_size must be >= 1");
+  if (p->causal != 0 && p->causal != 1) return fail(TILEMIX_ERR_SHAPE, "causal must be 0 or 1");
+  if (!(isfinite(p->scale) && p->scale > 0.0f))
+    return fail(TILEMIX_ERR_SHAPE, "scale must be finite and > 0");
+  if (p->route_per_batch != 0 && p->route_per_batch != 1)
+    return fail(TILEMIX_ERR_SHAPE, "route_per_batch must be 0 or 1");
+  if (p->route_hint != -1 && p->route_hint != 0)
+    return fail(TILEMIX_ERR_SHAPE, "route_hint must be -1 or 0");
+  const long long rows_q = (long long)p->batch * p->len_q * p->heads_q;
+  const long long rows_k = (long long)p->batch * p->len_k * p->heads_kv;
+  if (rows_q * p->head_dim > (1LL << 40) || rows_k * p->head_dim > (1LL << 40))
+    return fail(TILEMIX_ERR_SHAPE, "tensor too large");
+  const long long grid = (long long)p->batch * p->heads_q * cdiv(p->len_q, p->block_m);
+  if (grid > 0x7fffffffLL) return fail(TILEMIX_ERR_SHAPE, "too many query tiles");
+  if ((long long)p->heads_kv * p->batch > 65535 || p->heads_q > 65535)
+    return fail(TILEMIX_ERR_SHAPE, "too many heads");
+  return TILEMIX_OK;
+}
+
+Plan make_plan(const tilemix_params* p) {
+  Plan pl{};
+  pl.T_m = cdiv(p->len_q, p->block_m);
+  pl.T_n = cdiv(p->len_k, p->block_n);
+  pl.T_mask = cdiv(pl.T_n, p->group_size);
+  pl.W = cdiv(pl.T_mask, 64);
+  pl.nQB = cdiv(p->len_q, tilemix::kQuantBlockQ);
+  pl.nKB = cdiv(p->len_k, tilemix::kQuantBlockK);
+  const size_t d = (size_t)p->head_dim;
+  pl.q8_bytes = (size_t)p->batch * p->len_q * p->heads_q * d;
+  pl.k8_bytes = (size_t)p->batch * p->len_k * p->heads_kv * d;
+  pl.dq_bytes = (size_t)p->batch * pl.nQB * p->heads_q * 2;
+  pl.dk_bytes = (size_t)p->batch * pl.nKB * p->heads_kv * 2;
+  pl.vt_bytes = (size_t)p->batch * p->heads_kv * pl.T_n * d * tilemix::kBlockN * 2;
+  pl.q8_off = 0;
+  pl.k8_off = align256(pl.q8_off + pl.q8_bytes);
+  pl.dq_off = align256(pl.k8_off + pl.k8_bytes);
+  pl.dk_off = align256(pl.dq_off + pl.dq_bytes);
+  pl.vt_off = align256(pl.dk_off + pl.dk_bytes);
+  pl.total = align256(pl.vt_off + pl.vt_bytes);
+  return pl;
+}
+
+bool aligned(const void* ptr, size_t a) { return ((uintptr_t)ptr % a) == 0; }
+
+tilemix_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return TILEMIX_OK;
+  return fail(TILEMIX_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t tilemix_route_words_per_row(const tilemix_params* params) {
+  if (validate(params) != TILEMIX_OK) return 0;
+  return (int32_t)make_plan(params).W;
+}
+
+tilemix_status tilemix_workspace_size(const tilemix_params* params, size_t* bytes) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  if (!bytes) return fail(TILEMIX_ERR_NULL, "bytes is NULL");
+  *bytes = make_plan(params).total;
+  return ok();
+}
+
+namespace {
+
+tilemix_status check_workspace(const Plan& pl, const void* workspace, size_t workspace_bytes) {
+  if (!workspace) return fail(TILEMIX_ERR_WORKSPACE, "workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(TILEMIX_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (workspace_bytes < pl.total)
+    return fail(TILEMIX_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, pl.total);
+  return TILEMIX_OK;
+}
+
+tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void* Q, const void* K,
+                            const void* V, void* workspace, hipStream_t s) {
+  char* ws = static_cast<char*>(workspace);
+  int8_t* q8 = reinterpret_cast<int8_t*>(ws + pl.q8_off);
+  int8_t* k8 = reinterpret_cast<int8_t*>(ws + pl.k8_off);
+  uint16_t* dq = reinterpret_cast<uint16_t*>(ws + pl.dq_off);
+  uint16_t* dk = reinterpret_cast<uint16_t*>(ws + pl.dk_off);
+  _Float16* vt = reinterpret_cast<_Float16*>(ws + pl.vt_off);
+  tilemix_status st;
+  if (p.route_hint != 0) {   // an all-FP16 map skips the quantize-once pass
+    st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(Q), q8, dq, p.batch,
+                                             p.len_q, p.heads_q, p.head_dim,
+                                             tilemix::kQuantBlockQ, s), "quantize Q");
+    if (st != TILEMIX_OK) return st;
+    st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(K), k8, dk, p.batch,
+                                             p.len_k, p.heads_kv, p.head_dim,
+                                             tilemix::kQuantBlockK, s), "quantize K");
+    if (st != TILEMIX_OK) return st;
+  }
+  return hip_status(tilemix::launch_v_tiles(static_cast<const _Float16*>(V), vt, p.batch, p.len_k,
+                                            p.heads_kv, p.head_dim, s), "V tiles");
+}
+
+tilemix_status attend_impl(const tilemix_params& p, const Plan& pl, const void* Q, const void* K,
+                           const uint64_t* route_bits, void* O, const void* workspace,
+                           hipStream_t s) {
+  const char* ws = static_cast<const char*>(workspace);
+  tilemix::AttnArgs a{};
+  a.Q = static_cast<const _Float16*>(Q);
+  a.K = static_cast<const _Float16*>(K);
+  a.Vt = reinterpret_cast<const _Float16*>(ws + pl.vt_off);
+  a.Q8 = reinterpret_cast<const int8_t*>(ws + pl.q8_off);
+  a.K8 = reinterpret_cast<const int8_t*>(ws + pl.k8_off);
+  a.dQ = reinterpret_cast<const uint16_t*>(ws + pl.dq_off);
+  a.dK = reinterpret_cast<const uint16_t*>(ws + pl.dk_off);
+  a.route = route_bits;
+  a.O = static_cast<_Float16*>(O);
+  a.B = p.batch; a.Hq = p.heads_q; a.Hk = p.heads_kv; a.Lq = p.len_q; a.Lk = p.len_k;
+  a.T_m = (int)pl.T_m; a.T_n = (int)pl.T_n; a.W = (int)pl.W; a.g = p.group_size;
+  a.nQB = (int)pl.nQB; a.nKB = (int)pl.nKB;
+  a.causal = p.causal;
+  a.force_fp16 = p.route_hint == 0 ? 1 : 0;
+  a.route_batch_stride = p.route_per_batch ? (long long)p.heads_kv * pl.T_m * pl.W : 0;
+  a.scale_log2e = p.scale * 1.4426950408889634f;
+  return hip_status(tilemix::launch_routed_attention(a, p.head_dim, p.block_m, s), "routed attention");
+}
+
+tilemix_status check_qkv(const void* Q, const void* K, const void* V) {
+  if (!Q || !K || !V) return fail(TILEMIX_ERR_NULL, "Q, K and V must be non-NULL");
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16))
+    return fail(TILEMIX_ERR_ALIGN, "Q, K and V must be 16-byte aligned");
+  return TILEMIX_OK;
+}
+
+tilemix_status check_out(const uint64_t* route_bits, const void* O) {
+  if (!O || !route_bits) return fail(TILEMIX_ERR_NULL, "O and route_bits must be non-NULL");
+  if (!aligned(O, 16)) return fail(TILEMIX_ERR_ALIGN, "O must be 16-byte aligned");
+  if (!aligned(route_bits, 8)) return fail(TILEMIX_ERR_ALIGN, "route_bits must be 8-byte aligned");
+  return TILEMIX_OK;
+}
+
+}  // namespace
+
+tilemix_status tilemix_prefill(const tilemix_params* params, const void* Q, const void* K,
+                               const void* V, const uint64_t* route_bits, void* O,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
+  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
+  const Plan pl = make_plan(params);
+  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = prepare_impl(*params, pl, Q, K, V, workspace, s)) != TILEMIX_OK) return st;
+  if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, s)) != TILEMIX_OK) return st;
+  return ok();
+}
+
+tilemix_status tilemix_prepare(const tilemix_params* params, const void* Q, const void* K,
+                               const void* V, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
+  const Plan pl = make_plan(params);
+  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
+  if ((st = prepare_impl(*params, pl, Q, K, V, workspace, static_cast<hipStream_t>(stream))) != TILEMIX_OK)
+    return st;
+  return ok();
+}
+
+tilemix_status tilemix_attend(const tilemix_params* params, const void* Q, const void* K,
+                              const uint64_t* route_bits, void* O, const void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  if (!Q || !K) return fail(TILEMIX_ERR_NULL, "Q and K must be non-NULL");
+  if (!aligned(Q, 16) || !aligned(K, 16)) return fail(TILEMIX_ERR_ALIGN, "Q and K must be 16-byte aligned");
+  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
+  const Plan pl = make_plan(params);
+  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
+  if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, static_cast<hipStream_t>(stream))) != TILEMIX_OK)
+    return st;
+  return ok();
+}
+
+tilemix_status tilemix_quantize(const tilemix_params* params, const void* Q, const void* K,
+                                int8_t* Q8, uint16_t* dQ, int8_t* K8, uint16_t* dK, void* stream) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  const tilemix_params& p = *params;
+  if (!Q || !K || !Q8 || !dQ || !K8 || !dK) return fail(TILEMIX_ERR_NULL, "NULL tensor pointer");
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(Q8, 16) || !aligned(K8, 16) ||
+      !aligned(dQ, 2) || !aligned(dK, 2))
+    return fail(TILEMIX_ERR_ALIGN, "Q, K, Q8, K8 must be 16-byte and dQ, dK 2-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(Q), Q8, dQ, p.batch, p.len_q,
+                                           p.heads_q, p.head_dim, tilemix::kQuantBlockQ, s),
+                  "quantize Q");
+  if (st != TILEMIX_OK) return st;
+  st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(K), K8, dK, p.batch, p.len_k,
+                                           p.heads_kv, p.head_dim, tilemix::kQuantBlockK, s),
+                  "quantize K");
+  if (st != TILEMIX_OK) return st;
+  return ok();
+}
+
+tilemix_status tilemix_debug_qk_int32(const tilemix_params* params, const int8_t* Q8,
+                                      const int8_t* K8, const int32_t* tiles, int32_t count,
+                                      int32_t* out, void* stream) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  const tilemix_params& p = *params;
+  if (count < 0) return fail(TILEMIX_ERR_SHAPE, "count must be >= 0");
+  if (count == 0) return ok();
+  if (!Q8 || !K8 || !tiles || !out) return fail(TILEMIX_ERR_NULL, "NULL pointer");
+  if (!aligned(Q8, 16) || !aligned(K8, 16) || !aligned(tiles, 4) || !aligned(out, 4))
+    return fail(TILEMIX_ERR_ALIGN, "Q8, K8 must be 16-byte and tiles, out 4-byte aligned");
+  tilemix::DebugTileArgs a{};
+  a.Q8 = Q8; a.K8 = K8; a.tiles = tiles; a.out = out; a.count = count;
+  a.B = p.batch; a.Hq = p.heads_q; a.Hk = p.heads_kv; a.Lq = p.len_q; a.Lk = p.len_k;
+  st = hip_status(tilemix::launch_debug_tiles(a, p.head_dim, p.block_m, static_cast<hipStream_t>(stream)),
+                  "debug tiles");
+  if (st != TILEMIX_OK) return st;
+  return ok();
+}
+
+const char* tilemix_status_string(tilemix_status status) {
+  switch (status) {
+    case TILEMIX_OK: return "ok";
+    case TILEMIX_ERR_NULL: return "null pointer";
+    case TILEMIX_ERR_SHAPE: return "invalid shape or parameter";
+    case TILEMIX_ERR_UNSUPPORTED: return "unsupported configuration";
+    case TILEMIX_ERR_ALIGN: return "misaligned pointer";
+    case TILEMIX_ERR_WORKSPACE: return "workspace missing or too small";
+    case TILEMIX_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* tilemix_last_error(void) { return g_last_error; }
+
+}  // extern "C"

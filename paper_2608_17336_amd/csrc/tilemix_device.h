@@ -1,0 +1,80 @@
+// tilemix_device.h -- shared gfx950 device helpers for the TileMix kernels.
+//
+// Matrix-core shapes used (CDNA4 / gfx950, wave64):
+//   v_mfma_f32_32x32x16_f16 : A 32x16, B 16x32 FP16 -> D 32x32 FP32
+//   v_mfma_i32_32x32x32_i8  : A 32x32, B 32x32 INT8 -> D 32x32 INT32 (exact)
+// Operand lane layout (both shapes): lane l holds row/column (l % 32) and the
+// contraction slice [kw*(l/32), kw*(l/32)+kw) with kw = 8 (f16) or 16 (i8).
+// Accumulator layout: register r of lane l is D[8*(r/4) + 4*(l/32) + r%4][l%32].
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tilemix {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kQuantBlockQ = 128;  // query rows per INT8 scale block (Appendix C)
+constexpr int kQuantBlockK = 64;   // key rows per INT8 scale block (Appendix C)
+constexpr int kBlockN = 64;        // keys per compute tile (= key scale block)
+
+// Swizzled byte offset of 16-byte granule `c` in row `r` of an LDS tile whose rows are
+// `row_bytes` long.  Eight consecutive rows at the same logical granule land on eight
+// distinct 16-byte bank groups, so a ds_read_b128 of 8 consecutive lanes is conflict free.
+template <int ROW_BYTES>
+__device__ __forceinline__ int swz(int r, int c) {
+  if constexpr (ROW_BYTES >= 128) {
+    return r * ROW_BYTES + ((c ^ (r & 7)) << 4);
+  } else {
+    static_assert(ROW_BYTES == 64, "row size");
+    return r * ROW_BYTES + ((c ^ ((r >> 1) & 3)) << 4);
+  }
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
+  _Float16 v;
+  __builtin_memcpy(&v, &h, 2);
+  return (float)v;
+}
+
+// Value of lane (l ^ 32) of the same wave (the other half of a 32x32 accumulator column).
+__device__ __forceinline__ float other_half(float x) {
+  return __shfl_xor(x, 32, kWave);
+}
+
+__device__ __forceinline__ uint4 ld_global_16(const void* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+
+__device__ __forceinline__ void st_lds_16(char* lds, int off, uint4 v) {
+  *reinterpret_cast<uint4*>(lds + off) = v;
+}
+
+__device__ __forceinline__ uint4 ld_lds_16(const char* lds, int off) {
+  return *reinterpret_cast<const uint4*>(lds + off);
+}
+
+__device__ __forceinline__ half8 as_half8(uint4 v) { return __builtin_bit_cast(half8, v); }
+__device__ __forceinline__ i32x4 as_i32x4(uint4 v) { return __builtin_bit_cast(i32x4, v); }
+
+__device__ __forceinline__ f32x16 mfma_f16(half8 a, half8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ i32x16 mfma_i8(i32x4 a, i32x4 b, i32x16 c) {
+  return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+}
+
+// Key (row of the 32x32 accumulator block) held by register r of lane l.
+__device__ __forceinline__ int acc_row(int r, int lane) {
+  return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+
+}  // namespace tilemix

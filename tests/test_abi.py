@@ -1,0 +1,109 @@
+"""CPU checks of the C-ABI library: it loads, exports every declared symbol, and its host-side
+validation and workspace plan behave as include/tilemix.h states (no kernel is launched)."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2608_17336_amd as tm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tilemix.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(tm.library_path()),
+                                reason="libtilemix.so not built (run __graft_entry__.build())")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tilemix_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert _declared_functions() == sorted(tm.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = tm.load_library()
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", tm.library_path()], capture_output=True,
+                         text=True).stdout
+    for name in _declared_functions():
+        assert re.search(rf"\bT {name}$", out, re.M), name
+
+
+def _cp(**kw):
+    base = dict(batch=1, heads_q=32, heads_kv=8, len_q=8192, len_k=8192, head_dim=128,
+                block_m=128, block_n=64, group_size=1, causal=True, scale=0.0884)
+    base.update(kw)
+    return tm.Params(**base)
+
+
+def test_words_per_row():
+    assert tm.tilemix_route_words_per_row(_cp()) == 2                       # 128 groups
+    assert tm.tilemix_route_words_per_row(_cp(len_q=4096, len_k=4096)) == 1
+    assert tm.tilemix_route_words_per_row(_cp(len_q=131072, len_k=131072, group_size=16)) == 2
+    assert tm.tilemix_route_words_per_row(_cp(len_q=131072, len_k=131072, group_size=1)) == 32
+    assert tm.tilemix_route_words_per_row(_cp(head_dim=96)) == 0            # invalid -> 0
+
+
+def test_workspace_matches_quantize_once_accounting():
+    # H_q=32, H_k=8, L=8192, d=128: Q8 + K8 = 40 MiB; scales 64*32 + 128*8 FP16; V tiles = |V|
+    n = tm.tilemix_workspace_size(_cp())
+    q8 = 8192 * 32 * 128
+    k8 = 8192 * 8 * 128
+    scales = (64 * 32 + 128 * 8) * 2
+    vt = 8192 * 8 * 128 * 2
+    assert q8 + k8 == 40 * 2 ** 20
+    assert q8 + k8 + scales + vt <= n <= q8 + k8 + scales + vt + 5 * 256
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(heads_q=30), 2),          # H_q % H_k
+    (dict(head_dim=96), 3),
+    (dict(block_m=256), 3),
+    (dict(block_n=128), 3),
+    (dict(group_size=0), 2),
+    (dict(len_q=0), 2),
+    (dict(scale=-1.0), 2),
+    (dict(route_hint=1), 2),
+])
+def test_validation_errors(kw, status):
+    with pytest.raises(tm.TilemixError) as e:
+        tm.tilemix_workspace_size(_cp(**kw))
+    assert e.value.status == status
+    assert tm.load_library().tilemix_last_error().decode()
+
+
+def test_prefill_rejects_before_launch():
+    lib = tm.load_library()
+    cp = _cp().c()
+    # NULL tensors
+    st = lib.tilemix_prefill(ctypes.byref(cp), None, None, None, None, None, None, 0, None)
+    assert st == 1
+    # misaligned pointers (never dereferenced: validation fails first)
+    fake = ctypes.c_void_p(0x1001)
+    st = lib.tilemix_prefill(ctypes.byref(cp), fake, fake, fake, fake, fake, fake, 1 << 30, None)
+    assert st == 4
+    # workspace too small
+    ok = ctypes.c_void_p(0x100000)
+    st = lib.tilemix_prefill(ctypes.byref(cp), ok, ok, ok, ok, ok, ok, 1024, None)
+    assert st == 5
+    assert b"needed" in lib.tilemix_last_error()
+    # params NULL
+    assert lib.tilemix_prefill(None, ok, ok, ok, ok, ok, ok, 1 << 40, None) == 1
+    assert lib.tilemix_status_string(5) == b"workspace missing or too small"
+
+
+def test_debug_and_quantize_reject_before_launch():
+    lib = tm.load_library()
+    cp = _cp().c()
+    ok = ctypes.c_void_p(0x100000)
+    assert lib.tilemix_debug_qk_int32(ctypes.byref(cp), ok, ok, ok, -1, ok, None) == 2
+    assert lib.tilemix_debug_qk_int32(ctypes.byref(cp), ok, ok, ok, 0, ok, None) == 0   # nothing to do
+    assert lib.tilemix_quantize(ctypes.byref(cp), None, ok, ok, ok, ok, ok, None) == 1
