@@ -56,7 +56,7 @@ def cpu_baseline(cfg, Q, K, V, words, budget_rows=None):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = 1
-    stride = 64
+    stride = 32
     idx = np.arange(stride // 2, cfg.L, stride, dtype=np.int64)
     if budget_rows:
         idx = idx[:budget_rows]

@@ -121,13 +121,14 @@ def routed_attention_rows(Q, K, V, route_bits, *, block_m: int, block_n: int, gr
                 row_scores.append((keys, keys, np.zeros(0)))
                 continue
             bits = route_bits_for_keys(route_bits, b, h_k, int(i), keys, block_m, block_n, group_size)
+            sel = slice(int(keys[0]), int(keys[-1]) + 1)      # legal keys are one contiguous run
             q64 = Q[b, i, h_q, :].astype(np.float64)
-            s_fp16_path = scale * (k64[keys] @ q64)
-            c_int = k8[keys] @ operands.q8[b, i, h_q, :].astype(np.int64)        # exact int64
+            s_fp16_path = scale * (k64[sel] @ q64)
+            c_int = k8[sel] @ operands.q8[b, i, h_q, :].astype(np.int64)         # exact int64
             dq = np.float64(operands.dq[b, i // QUANT_BLOCK_Q, h_q])
             s_int8_path = scale * dq * dk[keys // QUANT_BLOCK_K] * c_int.astype(np.float64)
             s = np.where(bits == 1, s_int8_path, s_fp16_path)
-            o[t] = _softmax_output(s, v64[keys], d)
+            o[t] = _softmax_output(s, v64[sel], d)
             if want_scores:
                 row_scores.append((keys, bits, s))
         outs.append(o)

@@ -143,6 +143,7 @@ def test_unequal_lengths_bottom_right_causal():
 WL = [(name, mi) for name, cfg in WORKLOADS.items() for mi in range(len(cfg.masks))]
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", list(WORKLOADS))
 def test_workload_parity_sampled(name):
     cfg = WORKLOADS[name]
