@@ -23,6 +23,14 @@
 // the last legal key of the workgroup are never visited and waves whose rows see no
 // key of a tile skip its math.  Rows are scheduled longest-first, and consecutive
 // workgroups on one XCD share a KV head when the KV stream count allows it.
+//
+// Staging: tiles move HBM -> LDS by direct-to-LDS copies (global_load_lds_dwordx4), so no
+// registers hold the next tile.  Each LDS tile row (a key row of K or K8, a d row of V^T)
+// stores its 16-byte granules XOR-swizzled by the row index; each copying lane fetches the
+// source granule that belongs at its destination.  Eight consecutive rows read at one
+// logical granule then hit eight distinct bank groups.
+#include <type_traits>
+
 #include "tilemix_device.h"
 #include "tilemix_internal.h"
 
@@ -30,7 +38,6 @@ namespace tilemix {
 
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleThreshold = 8.0f;   // log2 units: rescale when the max grows > x256
 constexpr float kNegInf = -__builtin_huge_valf();
 
@@ -38,99 +45,107 @@ template <int D, int BM>
 struct TileCfg {
   static constexpr int kWaves = BM / 32;
   static constexpr int kThreads = kWaves * kWave;
-  static constexpr int kKBytes = kBlockN * D * 2;     // FP16 K tile (K8 uses half of it)
-  static constexpr int kVBytes = D * kBlockN * 2;     // V^T tile
+  static constexpr int kKRow = 2 * D;                 // LDS bytes per FP16 key row
+  static constexpr int kK8Row = D;                    // LDS bytes per INT8 key row
+  static constexpr int kVRow = 2 * kBlockN;           // LDS bytes per d row of V^T
+  static constexpr int kKBytes = kBlockN * kKRow;
+  static constexpr int kK8Bytes = kBlockN * kK8Row;
+  static constexpr int kVBytes = D * kVRow;
   static constexpr int kStage = kKBytes + kVBytes;
-  static constexpr int kKChunks = kKBytes / 16 / kThreads;   // 16-byte loads per thread
-  static constexpr int kK8Chunks = kKChunks / 2;
-  static constexpr int kVChunks = kVBytes / 16 / kThreads;
-  static_assert(kKChunks * kThreads * 16 == kKBytes, "K split");
-  static_assert(kK8Chunks * 2 == kKChunks, "K8 split");
-  static_assert(kVChunks * kThreads * 16 == kVBytes, "V split");
+  // 1 KB direct-to-LDS copies issued per wave for each tile kind
+  static constexpr int kKInstr = kKBytes / 1024 / kWaves;
+  static constexpr int kK8Instr = kK8Bytes / 1024 / kWaves;
+  static constexpr int kVInstr = kVBytes / 1024 / kWaves;
+  static_assert(kKInstr * kWaves * 1024 == kKBytes, "K split");
+  static_assert(kK8Instr * kWaves * 1024 == kK8Bytes, "K8 split");
+  static_assert(kVInstr * kWaves * 1024 == kVBytes, "V split");
 };
 
-// Registers holding one prefetched K/V tile on its way from HBM to LDS.
-template <int D, int BM>
-struct Prefetch {
-  uint4 k[TileCfg<D, BM>::kKChunks];
-  uint4 v[TileCfg<D, BM>::kVChunks];
-};
+// Row-swizzle key of an LDS tile row (see swz()).
+template <int ROW_BYTES>
+__device__ __forceinline__ int swz_key(int r) {
+  if constexpr (ROW_BYTES >= 128) return r & 7;
+  else return (r >> 1) & 3;
+}
 
-template <int D, int BM, bool WITH_V>
-__device__ __forceinline__ void load_tile(Prefetch<D, BM>& pf, const _Float16* __restrict__ K,
-                                          const int8_t* __restrict__ K8,
-                                          const _Float16* __restrict__ Vt, int b, int hk, int n,
-                                          int Lk, int Hk, int T_n, bool int8) {
-  using C = TileCfg<D, BM>;
-  const int tid = threadIdx.x;
-  const int key0 = n * kBlockN;
-  if (!int8) {
+// Direct-to-LDS copy plan of a tile with ROW_BYTES-byte rows: copy J (1 KB) has lane l write
+// LDS byte 1024*J + 16*l, i.e. row r = J*(1024/ROW_BYTES) + l/(ROW_BYTES/16) and swizzled
+// granule p = l % (ROW_BYTES/16); that slot holds logical granule c = p ^ swz_key(r), so the
+// lane reads source row r, granule c.  With 256-byte rows swz_key(r) depends on the parity of
+// J, otherwise not: the per-lane part of the source offset takes two values at most.
+template <int ROW_BYTES>
+struct DmaPlan {
+  static constexpr int kCpr = ROW_BYTES / 16;
+  static constexpr int kRowsPerCopy = 1024 / ROW_BYTES;
+  uint32_t off[2];   // lane part of the source byte offset for even / odd J
+  int row_in_copy;   // l / kCpr
+  __device__ __forceinline__ DmaPlan(int lane, int stride) {
+    row_in_copy = lane / kCpr;
 #pragma unroll
-    for (int i = 0; i < C::kKChunks; ++i) {
-      const int c = tid + C::kThreads * i;
-      const int row = c / (D / 8), ch = c % (D / 8);
-      const int key = key0 + row;
-      pf.k[i] = (key < Lk) ? ld_global_16(K + (((size_t)b * Lk + key) * Hk + hk) * D + ch * 8)
-                           : make_uint4(0, 0, 0, 0);
+    for (int par = 0; par < 2; ++par) {
+      const int r = par * kRowsPerCopy + row_in_copy;
+      const int c = (lane % kCpr) ^ swz_key<ROW_BYTES>(r);
+      off[par] = (uint32_t)row_in_copy * (uint32_t)stride + (uint32_t)c * 16u;
+    }
+  }
+};
+
+// Copy one tile into LDS.  `src` is the tile's first row (uniform), `stride` the bytes between
+// source rows, `rows_valid` how many of its rows exist: rows past it re-read the last valid
+// row, whose contents are never used unmasked.
+template <int ROW_BYTES, int INSTR, int ROWS>
+__device__ __forceinline__ void dma_tile(const char* src, int stride, int rows_valid, char* lds,
+                                         int wave, int lane, const DmaPlan<ROW_BYTES>& plan) {
+  constexpr int kRpc = DmaPlan<ROW_BYTES>::kRowsPerCopy;
+  if (rows_valid >= ROWS) {
+#pragma unroll
+    for (int j = 0; j < INSTR; ++j) {
+      const int J = wave * INSTR + j;
+      const char* s = src + (size_t)(J * kRpc) * stride;
+      dma_16(s + ((J & 1) ? plan.off[1] : plan.off[0]), lds + J * 1024);
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < C::kK8Chunks; ++i) {
-      const int c = tid + C::kThreads * i;
-      const int row = c / (D / 16), ch = c % (D / 16);
-      const int key = key0 + row;
-      pf.k[i] = (key < Lk) ? ld_global_16(K8 + (((size_t)b * Lk + key) * Hk + hk) * D + ch * 16)
-                           : make_uint4(0, 0, 0, 0);
-    }
-  }
-  if constexpr (WITH_V) {
-    const _Float16* vt = Vt + (((size_t)b * Hk + hk) * T_n + n) * (size_t)(D * kBlockN);
-#pragma unroll
-    for (int i = 0; i < C::kVChunks; ++i) {
-      const int c = tid + C::kThreads * i;
-      pf.v[i] = ld_global_16(vt + c * 8);
+    for (int j = 0; j < INSTR; ++j) {
+      const int J = wave * INSTR + j;
+      const int r = J * kRpc + plan.row_in_copy;
+      const int c = (lane % DmaPlan<ROW_BYTES>::kCpr) ^ swz_key<ROW_BYTES>(r);
+      const int rs = min(r, rows_valid - 1);
+      dma_16(src + (size_t)rs * stride + c * 16, lds + J * 1024);
     }
   }
 }
 
-template <int D, int BM, bool WITH_V>
-__device__ __forceinline__ void store_tile(const Prefetch<D, BM>& pf, char* stage, bool int8) {
-  using C = TileCfg<D, BM>;
-  const int tid = threadIdx.x;
-  if (!int8) {
+// Per-lane LDS fragment offsets for a swizzled tile with ROW_BYTES-byte rows: the 16-byte
+// granule 2*s + hi of row lq (+32 per block) is at frag[s & 3] + 32*(s & ~3).
+template <int ROW_BYTES>
+struct FragOffsets {
+  int o[4];
+  __device__ __forceinline__ explicit FragOffsets(int lane) {
+    const int lq = lane & 31, hi = lane >> 5;
+    if constexpr (ROW_BYTES >= 128) {
+      const int x1 = (lq >> 1) & 3;
 #pragma unroll
-    for (int i = 0; i < C::kKChunks; ++i) {
-      const int c = tid + C::kThreads * i;
-      st_lds_16(stage, swz<2 * D>(c / (D / 8), c % (D / 8)), pf.k[i]);
-    }
-  } else {
+      for (int u = 0; u < 4; ++u) o[u] = lq * ROW_BYTES + 16 * (hi ^ (lq & 1)) + 32 * (u ^ x1);
+    } else {
+      const int y = (lq >> 1) & 3;
 #pragma unroll
-    for (int i = 0; i < C::kK8Chunks; ++i) {
-      const int c = tid + C::kThreads * i;
-      st_lds_16(stage, swz<D>(c / (D / 16), c % (D / 16)), pf.k[i]);
-    }
-  }
-  if constexpr (WITH_V) {
-    char* vs = stage + C::kKBytes;
-#pragma unroll
-    for (int i = 0; i < C::kVChunks; ++i) {
-      const int c = tid + C::kThreads * i;
-      st_lds_16(vs, swz<128>(c / 8, c % 8), pf.v[i]);
+      for (int u = 0; u < 4; ++u) o[u] = lq * ROW_BYTES + 16 * (hi ^ (y & 1)) + 32 * ((u & 1) ^ (y >> 1));
     }
   }
-}
+  __device__ __forceinline__ int at(int s) const { return o[s & 3] + 32 * (s & ~3); }
+};
 
 // S^T tile (64 keys x 32 queries of this wave) by the INT8 route: exact INT32 products.
 template <int D>
-__device__ __forceinline__ void qk_int8(const char* kst, const i32x4 (&q8f)[D / 32], int lane,
-                                        i32x16& acc0, i32x16& acc1) {
-  const int lq = lane & 31, hi = lane >> 5;
+__device__ __forceinline__ void qk_int8(const char* kst, const FragOffsets<D>& fo,
+                                        const i32x4 (&q8f)[D / 32], i32x16& acc0, i32x16& acc1) {
   acc0 = i32x16{};
   acc1 = i32x16{};
 #pragma unroll
   for (int s = 0; s < D / 32; ++s) {
-    const i32x4 a0 = as_i32x4(ld_lds_16(kst, swz<D>(lq, 2 * s + hi)));
-    const i32x4 a1 = as_i32x4(ld_lds_16(kst, swz<D>(32 + lq, 2 * s + hi)));
+    const i32x4 a0 = as_i32x4(ld_lds_16(kst, fo.at(s)));
+    const i32x4 a1 = as_i32x4(ld_lds_16(kst, fo.at(s) + 32 * D));
     acc0 = mfma_i8(a0, q8f[s], acc0);
     acc1 = mfma_i8(a1, q8f[s], acc1);
   }
@@ -138,18 +153,76 @@ __device__ __forceinline__ void qk_int8(const char* kst, const i32x4 (&q8f)[D / 
 
 // S^T tile by the FP16 route: FP16 products, FP32 accumulation.
 template <int D>
-__device__ __forceinline__ void qk_fp16(const char* kst, const half8 (&qf)[D / 16], int lane,
-                                        f32x16& acc0, f32x16& acc1) {
-  const int lq = lane & 31, hi = lane >> 5;
+__device__ __forceinline__ void qk_fp16(const char* kst, const FragOffsets<2 * D>& fo,
+                                        const half8 (&qf)[D / 16], f32x16& acc0, f32x16& acc1) {
   acc0 = f32x16{};
   acc1 = f32x16{};
 #pragma unroll
   for (int s = 0; s < D / 16; ++s) {
-    const half8 a0 = as_half8(ld_lds_16(kst, swz<2 * D>(lq, 2 * s + hi)));
-    const half8 a1 = as_half8(ld_lds_16(kst, swz<2 * D>(32 + lq, 2 * s + hi)));
+    const half8 a0 = as_half8(ld_lds_16(kst, fo.at(s)));
+    const half8 a1 = as_half8(ld_lds_16(kst, fo.at(s) + 32 * 2 * D));
     acc0 = mfma_f16(a0, qf[s], acc0);
     acc1 = mfma_f16(a1, qf[s], acc1);
   }
+}
+
+// One online-softmax step (Section 3.1) for the 64 scores a lane holds.  `sv` are raw
+// scores (INT32 products or FP16-route dot products); `c` turns them into log2-domain
+// scaled scores.  Produces P in FP16, packed in P.V operand order, and updates the state.
+template <int D, bool MASKED>
+__device__ __forceinline__ void softmax_step(float (&sv)[32], float c, int key0, int last_key,
+                                             int lane, float& m_run, float& z_run,
+                                             f32x16 (&oacc)[D / 32], half8 (&pfr)[4]) {
+  float mt;
+  if constexpr (MASKED) {
+    // Scale first, then mask, so a zero scale can never meet an infinity.  Element i is key
+    // key0 + 32*(i/16) + acc_row(i%16, lane); only the 4*(lane/32) part depends on the lane.
+    const int lim = last_key - key0 - 4 * (lane >> 5);
+    float mx = kNegInf;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const int kc = 32 * (i >> 4) + 8 * ((i & 15) >> 2) + (i & 3);
+      sv[i] = kc <= lim ? sv[i] * c : kNegInf;
+      mx = fmaxf(mx, sv[i]);
+    }
+    mt = pair_max(mx);
+  } else {
+    float mx = sv[0];
+#pragma unroll
+    for (int i = 1; i < 32; ++i) mx = fmaxf(mx, sv[i]);
+    mt = pair_max(mx) * c;
+  }
+  const float m_new = fmaxf(m_run, mt);
+  if (__any(m_new > m_run + kRescaleThreshold)) {
+    const float alpha = (m_new == kNegInf) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+    z_run *= alpha;
+#pragma unroll
+    for (int cc = 0; cc < D / 32; ++cc) oacc[cc] *= alpha;
+    m_run = m_new;
+  }
+  const float msub = (m_run == kNegInf) ? 0.0f : m_run;
+  float zs = 0.0f;
+  const half2v ones = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const int i = 16 * (t >> 1) + 8 * (t & 1) + e;
+      float p0, p1;
+      if constexpr (MASKED) {
+        p0 = __builtin_amdgcn_exp2f(sv[i] - msub);
+        p1 = __builtin_amdgcn_exp2f(sv[i + 1] - msub);
+      } else {
+        p0 = __builtin_amdgcn_exp2f(fmaf(sv[i], c, -msub));
+        p1 = __builtin_amdgcn_exp2f(fmaf(sv[i + 1], c, -msub));
+      }
+      const half2v pr = {(_Float16)p0, (_Float16)p1};
+      zs = __builtin_amdgcn_fdot2(pr, ones, zs, false);
+      pfr[t][e] = pr[0];
+      pfr[t][e + 1] = pr[1];
+    }
+  }
+  z_run += zs;
 }
 
 // Map a linear workgroup id to (b, h_q, m): rows longest first (largest m first for causal
@@ -180,6 +253,13 @@ __device__ __forceinline__ void decode_unit(int id, int B, int Hq, int Hk, int T
   hq = hk * G + qg;
 }
 
+__device__ __forceinline__ float load_scale_uniform(const uint16_t* base, size_t idx) {
+  // The scale arrays live in 256-byte aligned workspace slots, so reading the aligned
+  // 32-bit word that holds element idx stays inside the slot.
+  const uint32_t w = reinterpret_cast<const uint32_t*>(base)[idx >> 1];
+  return half_bits_to_float((uint16_t)((idx & 1) ? (w >> 16) : (w & 0xffffu)));
+}
+
 template <int D, int BM>
 __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) {
   using C = TileCfg<D, BM>;
@@ -189,22 +269,25 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
   decode_unit(blockIdx.x, a.B, a.Hq, a.Hk, a.T_m, b, hq, hk, m);
 
   const int tid = threadIdx.x;
-  const int wave = tid / kWave, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & (kWave - 1);
   const int lq = lane & 31, hi = lane >> 5;
   const int q0 = m * BM + 32 * wave;          // first query row of this wave
   const int my_q = q0 + lq;
-  const int off = a.Lk - a.Lq;                // bottom-right causal alignment
+  // Row i may see keys j <= i + off (bottom-right causal alignment); without the causal
+  // mask every key up to L_k - 1 is legal.
+  const int off = a.causal ? a.Lk - a.Lq : a.Lk;
   const bool wave_active = q0 < a.Lq;
 
   // Last key any row of the workgroup / of this wave may see.
-  const int wg_last_q = min(a.Lq - 1, m * BM + BM - 1);
-  int wg_last_key = a.causal ? min(a.Lk - 1, wg_last_q + off) : a.Lk - 1;
-  const int wave_last_q = min(a.Lq - 1, q0 + 31);
-  const int wave_last_key = a.causal ? min(a.Lk - 1, wave_last_q + off) : a.Lk - 1;
+  const int wg_last_key = min(a.Lk - 1, min(a.Lq - 1, m * BM + BM - 1) + off);
+  const int wave_last_key = min(a.Lk - 1, min(a.Lq - 1, q0 + 31) + off);
+  const int first_row_last_key = min(a.Lk - 1, q0 + off);    // smallest last key of the wave
+  const int my_last_key = min(a.Lk - 1, my_q + off);
 
   _Float16* orow = a.O + (((size_t)b * a.Lq + my_q) * a.Hq + hq) * D;
   if (wg_last_key < 0) {   // no legal key for any row of this tile: output is zero
-    if (my_q < a.Lq) {   // the two lanes of a row each clear half of it
+    if (my_q < a.Lq) {     // the two lanes of a row each clear half of it
 #pragma unroll
       for (int c = 0; c < D / 2; c += 8) *reinterpret_cast<half8*>(orow + hi * (D / 2) + c) = half8{};
     }
@@ -245,8 +328,35 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
   for (int s = 0; s < D / 32; ++s)
     q8f[s] = (need_int8 && row_ok) ? as_i32x4(ld_global_16(a.Q8 + qoff + 32 * s + 16 * hi)) : i32x4{};
   const float dq = (need_int8 && wave_active)
-                       ? half_bits_to_float(a.dQ[((size_t)b * a.nQB + q0 / kQuantBlockQ) * a.Hq + hq])
+                       ? load_scale_uniform(a.dQ, ((size_t)b * a.nQB + q0 / kQuantBlockQ) * a.Hq + hq)
                        : 0.0f;
+  const float c_fp16 = a.scale_log2e;
+  const float c_int8_q = a.scale_log2e * dq;
+
+  // Tile sources (uniform bases) and per-lane LDS fragment offsets.
+  const int kstride = a.Hk * D * 2;                              // bytes between keys (FP16)
+  const char* kbase = reinterpret_cast<const char*>(a.K) + ((size_t)b * a.Lk * a.Hk + hk) * D * 2;
+  const char* k8base = reinterpret_cast<const char*>(a.K8) + ((size_t)b * a.Lk * a.Hk + hk) * D;
+  const char* vbase = reinterpret_cast<const char*>(a.Vt) +
+                      ((size_t)b * a.Hk + hk) * a.T_n * (size_t)(D * kBlockN * 2);
+  const DmaPlan<C::kKRow> plan_k(lane, kstride);
+  const DmaPlan<C::kK8Row> plan_k8(lane, kstride / 2);
+  const DmaPlan<C::kVRow> plan_v(lane, C::kVRow);
+  auto issue = [&](int n, bool int8) {   // start copying key tile n into stage n & 1
+    char* st = smem + (n & 1) * C::kStage;
+    const int rows = min(kBlockN, a.Lk - n * kBlockN);
+    if (int8)
+      dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(k8base + (size_t)n * kBlockN * (kstride / 2),
+                                                kstride / 2, rows, st, wave, lane, plan_k8);
+    else
+      dma_tile<C::kKRow, C::kKInstr, kBlockN>(kbase + (size_t)n * kBlockN * kstride, kstride, rows,
+                                              st, wave, lane, plan_k);
+    dma_tile<C::kVRow, C::kVInstr, D>(vbase + (size_t)n * (D * kBlockN * 2), C::kVRow, D,
+                                      st + C::kKBytes, wave, lane, plan_v);
+  };
+  const FragOffsets<C::kKRow> fo_k(lane);
+  const FragOffsets<C::kK8Row> fo_k8(lane);
+  const FragOffsets<C::kVRow> fo_v(lane);
 
   // Online-softmax state (Section 3.1), FP32; max kept in log2 units.
   float m_run = kNegInf;
@@ -255,135 +365,87 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
 #pragma unroll
   for (int c = 0; c < D / 32; ++c) oacc[c] = f32x16{};
 
-  Prefetch<D, BM> pf;
   bool r_cur = route_of(0);
-  load_tile<D, BM, true>(pf, a.K, a.K8, a.Vt, b, hk, 0, a.Lk, a.Hk, a.T_n, r_cur);
-  store_tile<D, BM, true>(pf, smem, r_cur);
+  issue(0, r_cur);
+  wait_vmem();
   __syncthreads();
 
-  for (int n = 0; n <= n_end; ++n) {
-    char* kst = smem + (n & 1) * C::kStage;
+  // One key tile: prefetch tile n + 1, compute tile n, publish the prefetch.  MASKED tiles
+  // apply the causal / sequence-end mask; they are the tiles past the first key tile that
+  // some row of the workgroup cannot fully see, and run in a loop of their own so the
+  // unmasked loop stays lean.
+  auto step = [&](int n, auto masked_tag) {
+    constexpr bool kMasked = decltype(masked_tag)::value;
+    const char* kst = smem + (n & 1) * C::kStage;
     const char* vst = kst + C::kKBytes;
     const bool has_next = n < n_end;
     bool r_next = false;
     if (has_next) {
       r_next = route_of(n + 1);
-      load_tile<D, BM, true>(pf, a.K, a.K8, a.Vt, b, hk, n + 1, a.Lk, a.Hk, a.T_n, r_next);
+      issue(n + 1, r_next);
     }
-
     const int key0 = n * kBlockN;
-    if (wave_active && key0 <= wave_last_key) {
+    if (wave_active && (!kMasked || key0 <= wave_last_key)) {
       float sv[32];
       float c;   // factor from raw score to log2-domain scaled score
       if (r_cur) {
         i32x16 i0, i1;
-        qk_int8<D>(kst, q8f, lane, i0, i1);
+        qk_int8<D>(kst, fo_k8, q8f, i0, i1);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           sv[r] = (float)i0[r];
           sv[16 + r] = (float)i1[r];
         }
-        const float dk = half_bits_to_float(a.dK[((size_t)b * a.nKB + n) * a.Hk + hk]);
-        c = a.scale_log2e * dq * dk;
+        c = c_int8_q * load_scale_uniform(a.dK, ((size_t)b * a.nKB + n) * a.Hk + hk);
       } else {
         f32x16 f0, f1;
-        qk_fp16<D>(kst, qf, lane, f0, f1);
+        qk_fp16<D>(kst, fo_k, qf, f0, f1);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           sv[r] = f0[r];
           sv[16 + r] = f1[r];
         }
-        c = a.scale_log2e;
+        c = c_fp16;
       }
-
-      // Row max of this tile, in the log2 domain.
-      const bool masked = (key0 + kBlockN - 1 > (a.causal ? q0 + off : a.Lk - 1)) ||
-                          (key0 + kBlockN > a.Lk);
-      float mt;
-      if (masked) {
-        // Scale first, then mask, so a zero scale can never meet an infinity.
-        float mx = kNegInf;
-#pragma unroll
-        for (int i = 0; i < 32; ++i) {
-          const int key = key0 + 32 * (i >> 4) + acc_row(i & 15, lane);
-          const bool legal = key < a.Lk && (!a.causal || key <= my_q + off);
-          sv[i] = legal ? sv[i] * c : kNegInf;
-          mx = fmaxf(mx, sv[i]);
-        }
-        mt = fmaxf(mx, other_half(mx));
-      } else {
-        float mx = sv[0];
-#pragma unroll
-        for (int i = 1; i < 32; ++i) mx = fmaxf(mx, sv[i]);
-        mx = fmaxf(mx, other_half(mx));
-        mt = mx * c;
-      }
-
-      const float m_new = fmaxf(m_run, mt);
-      const bool grow = m_new > m_run + kRescaleThreshold;
-      if (__any(grow)) {
-        const float alpha = (m_new == kNegInf) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
-        z_run *= alpha;
-#pragma unroll
-        for (int cc = 0; cc < D / 32; ++cc) oacc[cc] *= alpha;
-        m_run = m_new;
-      }
-      const float msub = (m_run == kNegInf) ? 0.0f : m_run;
-
-      // P = exp2(s*c - m), packed to FP16 in the P.V operand order; z += sum(P) (of the
-      // FP16 values actually multiplied into V).
       half8 pfr[4];
-      float zs = 0.0f;
-      const half2v ones = {(_Float16)1.0f, (_Float16)1.0f};
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const int i = 16 * (t >> 1) + 8 * (t & 1) + e;
-          float p0, p1;
-          if (masked) {
-            p0 = __builtin_amdgcn_exp2f(sv[i] - msub);
-            p1 = __builtin_amdgcn_exp2f(sv[i + 1] - msub);
-          } else {
-            p0 = __builtin_amdgcn_exp2f(fmaf(sv[i], c, -msub));
-            p1 = __builtin_amdgcn_exp2f(fmaf(sv[i + 1], c, -msub));
-          }
-          const half2v pr = {(_Float16)p0, (_Float16)p1};
-          zs = __builtin_amdgcn_fdot2(pr, ones, zs, false);
-          pfr[t][e] = pr[0];
-          pfr[t][e + 1] = pr[1];
-        }
-      }
-      z_run += zs;
+      softmax_step<D, kMasked>(sv, c, key0, my_last_key, lane, m_run, z_run, oacc, pfr);
 
-      // O^T += V^T P^T
+      // O^T += V^T P^T: granule 2t + hi of V^T row 32*cc + lq holds the keys of P^T slot t.
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
 #pragma unroll
         for (int cc = 0; cc < D / 32; ++cc) {
-          const half8 va = as_half8(ld_lds_16(vst, swz<128>(32 * cc + lq, 2 * t + hi)));
+          const half8 va = as_half8(ld_lds_16(vst, fo_v.at(t) + cc * 32 * C::kVRow));
           oacc[cc] = mfma_f16(va, pfr[t], oacc[cc]);
         }
       }
     }
-
-    if (has_next) store_tile<D, BM, true>(pf, smem + ((n + 1) & 1) * C::kStage, r_next);
-    __syncthreads();
+    wait_vmem();       // the copies of tile n + 1 have landed in LDS
+    __syncthreads();   // ... for every wave, and every wave is done reading tile n
     r_cur = r_next;
-  }
+  };
+
+  // Tiles whose every key every row of the workgroup may see: keys <= the first row's last key.
+  const int wg_first_row_last_key = min(a.Lk - 1, m * BM + off);
+  const int n_split = max(0, min(n_end + 1, (wg_first_row_last_key + 1) / kBlockN));
+  int n = 0;
+  for (; n < n_split; ++n) step(n, std::integral_constant<bool, false>{});
+  for (; n <= n_end; ++n) step(n, std::integral_constant<bool, true>{});
 
   // Epilogue: O = O~ / z~, FP16 (round to nearest even).
-  if (wave_active && row_ok) {
-    const float zt = z_run + other_half(z_run);
+  if (wave_active) {
+    const float zt = pair_sum(z_run);
     const float inv = zt > 0.0f ? 1.0f / zt : 0.0f;
+    if (row_ok) {
 #pragma unroll
-    for (int cc = 0; cc < D / 32; ++cc) {
+      for (int cc = 0; cc < D / 32; ++cc) {
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        half4 h;
+        for (int rg = 0; rg < 4; ++rg) {
+          half4 h;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) h[e] = (_Float16)(oacc[cc][4 * rg + e] * inv);
-        *reinterpret_cast<half4*>(orow + 32 * cc + 8 * rg + 4 * hi) = h;
+          for (int e = 0; e < 4; ++e) h[e] = (_Float16)(oacc[cc][4 * rg + e] * inv);
+          *reinterpret_cast<half4*>(orow + 32 * cc + 8 * rg + 4 * hi) = h;
+        }
       }
     }
   }
@@ -399,7 +461,8 @@ __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
   const int b = a.tiles[4 * e + 0], hq = a.tiles[4 * e + 1];
   const int m = a.tiles[4 * e + 2], n = a.tiles[4 * e + 3];
   const int tid = threadIdx.x;
-  const int wave = tid / kWave, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & (kWave - 1);
   const int lq = lane & 31, hi = lane >> 5;
   int32_t* out = a.out + (size_t)e * BM * kBlockN;
   const bool ok = b >= 0 && b < a.B && hq >= 0 && hq < a.Hq && m >= 0 && n >= 0 &&
@@ -409,9 +472,13 @@ __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
     return;
   }
   const int hk = hq / (a.Hq / a.Hk);
-  Prefetch<D, BM> pf;
-  load_tile<D, BM, false>(pf, nullptr, a.K8, nullptr, b, hk, n, a.Lk, a.Hk, 0, true);
-  store_tile<D, BM, false>(pf, smem, true);
+  const int kstride = a.Hk * D * 2;
+  const char* k8t = reinterpret_cast<const char*>(a.K8) +
+                    ((size_t)b * a.Lk * a.Hk + hk) * D + (size_t)n * kBlockN * (kstride / 2);
+  const int rows = min(kBlockN, a.Lk - n * kBlockN);
+  const DmaPlan<C::kK8Row> plan_k8(lane, kstride / 2);
+  dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(k8t, kstride / 2, rows, smem, wave, lane, plan_k8);
+  wait_vmem();
   __syncthreads();
   const int my_q = m * BM + 32 * wave + lq;
   i32x4 q8f[D / 32];
@@ -419,13 +486,15 @@ __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
 #pragma unroll
   for (int s = 0; s < D / 32; ++s)
     q8f[s] = (my_q < a.Lq) ? as_i32x4(ld_global_16(a.Q8 + qoff + 32 * s + 16 * hi)) : i32x4{};
+  const FragOffsets<C::kK8Row> fo_k8(lane);
   i32x16 i0, i1;
-  qk_int8<D>(smem, q8f, lane, i0, i1);
+  qk_int8<D>(smem, fo_k8, q8f, i0, i1);
   const int row = 32 * wave + lq;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    out[row * kBlockN + acc_row(r, lane)] = i0[r];
-    out[row * kBlockN + 32 + acc_row(r, lane)] = i1[r];
+    const int k0 = acc_row(r, lane), k1 = 32 + acc_row(r, lane);
+    out[row * kBlockN + k0] = k0 < rows ? i0[r] : 0;      // keys past L_k: 0
+    out[row * kBlockN + k1] = k1 < rows ? i1[r] : 0;
   }
 }
 

@@ -25,29 +25,38 @@ constexpr int kQuantBlockQ = 128;  // query rows per INT8 scale block (Appendix 
 constexpr int kQuantBlockK = 64;   // key rows per INT8 scale block (Appendix C)
 constexpr int kBlockN = 64;        // keys per compute tile (= key scale block)
 
-// Swizzled byte offset of 16-byte granule `c` in row `r` of an LDS tile whose rows are
-// `row_bytes` long.  Eight consecutive rows at the same logical granule land on eight
-// distinct 16-byte bank groups, so a ds_read_b128 of 8 consecutive lanes is conflict free.
-template <int ROW_BYTES>
-__device__ __forceinline__ int swz(int r, int c) {
-  if constexpr (ROW_BYTES >= 128) {
-    return r * ROW_BYTES + ((c ^ (r & 7)) << 4);
-  } else {
-    static_assert(ROW_BYTES == 64, "row size");
-    return r * ROW_BYTES + ((c ^ ((r >> 1) & 3)) << 4);
-  }
-}
-
 __device__ __forceinline__ float half_bits_to_float(uint16_t h) {
   _Float16 v;
   __builtin_memcpy(&v, &h, 2);
   return (float)v;
 }
 
-// Value of lane (l ^ 32) of the same wave (the other half of a 32x32 accumulator column).
-__device__ __forceinline__ float other_half(float x) {
-  return __shfl_xor(x, 32, kWave);
+// Lanes l and l^32 of a 32x32 accumulator column hold the same query row.  After
+// v_permlane32_swap with both operands equal to x, the two results of every lane are
+// {x[l], x[l ^ 32]} (in lane-dependent order), so their max / sum is the pair value.
+__device__ __forceinline__ float pair_max(float x) {
+  const int v = __builtin_bit_cast(int, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__builtin_bit_cast(float, (int)r[0]), __builtin_bit_cast(float, (int)r[1]));
 }
+
+__device__ __forceinline__ float pair_sum(float x) {
+  const int v = __builtin_bit_cast(int, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __builtin_bit_cast(float, (int)r[0]) + __builtin_bit_cast(float, (int)r[1]);
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void global_void_t;
+
+// Direct global -> LDS copy of 16 bytes per lane: lane l of the wave writes
+// lds_wave_base + 16*l (lds_wave_base must be wave-uniform).  Completion is tracked by
+// vmcnt like any vector load.
+__device__ __forceinline__ void dma_16(const void* src, char* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((global_void_t*)src, (lds_void_t*)lds_wave_base, 16, 0, 0);
+}
+
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 __device__ __forceinline__ uint4 ld_global_16(const void* p) {
   return *reinterpret_cast<const uint4*>(p);
