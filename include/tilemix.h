@@ -70,7 +70,7 @@ typedef struct tilemix_params {
   int32_t heads_q;        /* H_q >= 1 */
   int32_t heads_kv;       /* H_k >= 1 and H_q % H_k == 0 */
   int32_t len_q;          /* L_q >= 1 */
-  int32_t len_k;          /* L_k >= 1 */
+  int32_t len_k;          /* 1 <= L_k <= 262144 */
   int32_t head_dim;       /* d: 64 or 128 */
   int32_t block_m;        /* BLOCK_M (query rows per routed tile): 64 or 128 */
   int32_t block_n;        /* BLOCK_N (keys per routed tile): 64 */

@@ -25,10 +25,13 @@
 // workgroups on one XCD share a KV head when the KV stream count allows it.
 //
 // Staging: tiles move HBM -> LDS by direct-to-LDS copies (global_load_lds_dwordx4), so no
-// registers hold the next tile.  Each LDS tile row (a key row of K or K8, a d row of V^T)
-// stores its 16-byte granules XOR-swizzled by the row index; each copying lane fetches the
-// source granule that belongs at its destination.  Eight consecutive rows read at one
-// logical granule then hit eight distinct bank groups.
+// registers hold the next tile.  Every LDS tile is made of 128-byte rows (an FP16 key tile
+// of d = 128 is stored as two 64-row halves, one per 64 channels) whose 16-byte granules are
+// XOR-swizzled by (row / 2) mod 8; each copying lane fetches the source granule that belongs
+// at its destination.  gfx950's LDS serves 16 lanes of a 16-byte read per cycle over 64
+// banks: those 16 lanes read 16 consecutive rows at one logical granule, and the swizzle
+// spreads them over all 64 banks.  INT8 key tiles of d = 64 use 64-byte rows swizzled by
+// (row / 4) mod 4 to the same effect.
 #include <type_traits>
 
 #include "tilemix_device.h"
@@ -41,14 +44,17 @@ namespace {
 constexpr float kRescaleThreshold = 8.0f;   // log2 units: rescale when the max grows > x256
 constexpr float kNegInf = -__builtin_huge_valf();
 
-template <int D, int BM>
+template <int D, int BM, int HEADS>
 struct TileCfg {
-  static constexpr int kWaves = BM / 32;
+  static constexpr int kWavesPerHead = BM / 32;
+  static constexpr int kWaves = HEADS * kWavesPerHead;
   static constexpr int kThreads = kWaves * kWave;
-  static constexpr int kKRow = 2 * D;                 // LDS bytes per FP16 key row
+  static constexpr int kKHalves = D / 64;             // FP16 key tile: 64-channel halves
+  static constexpr int kKRow = 128;                   // LDS bytes per FP16 key row (one half)
   static constexpr int kK8Row = D;                    // LDS bytes per INT8 key row
   static constexpr int kVRow = 2 * kBlockN;           // LDS bytes per d row of V^T
-  static constexpr int kKBytes = kBlockN * kKRow;
+  static constexpr int kKHalfBytes = kBlockN * kKRow;
+  static constexpr int kKBytes = kKHalves * kKHalfBytes;
   static constexpr int kK8Bytes = kBlockN * kK8Row;
   static constexpr int kVBytes = D * kVRow;
   static constexpr int kStage = kKBytes + kVBytes;
@@ -61,79 +67,84 @@ struct TileCfg {
   static_assert(kVInstr * kWaves * 1024 == kVBytes, "V split");
 };
 
-// Row-swizzle key of an LDS tile row (see swz()).
+// Row-swizzle key of an LDS tile row: granule c of row r is stored at granule c ^ key(r).
 template <int ROW_BYTES>
 __device__ __forceinline__ int swz_key(int r) {
-  if constexpr (ROW_BYTES >= 128) return r & 7;
-  else return (r >> 1) & 3;
+  static_assert(ROW_BYTES == 128 || ROW_BYTES == 64, "row size");
+  if constexpr (ROW_BYTES == 128) return (r >> 1) & 7;
+  else return (r >> 2) & 3;
 }
 
 // Direct-to-LDS copy plan of a tile with ROW_BYTES-byte rows: copy J (1 KB) has lane l write
 // LDS byte 1024*J + 16*l, i.e. row r = J*(1024/ROW_BYTES) + l/(ROW_BYTES/16) and swizzled
 // granule p = l % (ROW_BYTES/16); that slot holds logical granule c = p ^ swz_key(r), so the
-// lane reads source row r, granule c.  With 256-byte rows swz_key(r) depends on the parity of
-// J, otherwise not: the per-lane part of the source offset takes two values at most.
+// lane reads source row r, granule c.  swz_key(r) depends on the parity of J for 128-byte
+// rows, not for 64-byte rows: the per-lane part of the source offset takes two values at most.
 template <int ROW_BYTES>
 struct DmaPlan {
   static constexpr int kCpr = ROW_BYTES / 16;
   static constexpr int kRowsPerCopy = 1024 / ROW_BYTES;
-  uint32_t off[2];   // lane part of the source byte offset for even / odd J
-  int row_in_copy;   // l / kCpr
+  uint32_t off_even, off_odd;   // lane part of the source byte offset for even / odd J
+  int row_in_copy;              // l / kCpr
   __device__ __forceinline__ DmaPlan(int lane, int stride) {
     row_in_copy = lane / kCpr;
-#pragma unroll
-    for (int par = 0; par < 2; ++par) {
-      const int r = par * kRowsPerCopy + row_in_copy;
-      const int c = (lane % kCpr) ^ swz_key<ROW_BYTES>(r);
-      off[par] = (uint32_t)row_in_copy * (uint32_t)stride + (uint32_t)c * 16u;
-    }
+    off_even = lane_offset(lane, stride, 0);
+    off_odd = lane_offset(lane, stride, 1);
+  }
+  __device__ __forceinline__ uint32_t lane_offset(int lane, int stride, int par) const {
+    const int r = par * kRowsPerCopy + row_in_copy;
+    const int c = (lane % kCpr) ^ swz_key<ROW_BYTES>(r);
+    return (uint32_t)row_in_copy * (uint32_t)stride + (uint32_t)c * 16u;
   }
 };
 
 // Copy one tile into LDS.  `src` is the tile's first row (uniform), `stride` the bytes between
 // source rows, `rows_valid` how many of its rows exist: rows past it re-read the last valid
-// row, whose contents are never used unmasked.
-template <int ROW_BYTES, int INSTR, int ROWS>
-__device__ __forceinline__ void dma_tile(const char* src, int stride, int rows_valid, char* lds,
-                                         int wave, int lane, const DmaPlan<ROW_BYTES>& plan) {
+// row, whose contents are never used unmasked.  Copies come in blocks of BLOCK_COPIES; block k
+// covers source columns [k*COL_STEP, (k+1)*COL_STEP) of the same rows (the channel halves of
+// an FP16 key tile) and lands right after block k-1 in LDS.
+template <int ROW_BYTES, int INSTR, int ROWS, int BLOCK_COPIES = (1 << 20), int COL_STEP = 0>
+__device__ __forceinline__ void dma_tile(const char* src, int stride, int rows_valid, uint32_t lds,
+                                         int wave, int lane, const DmaPlan<ROW_BYTES> plan) {
   constexpr int kRpc = DmaPlan<ROW_BYTES>::kRowsPerCopy;
   if (rows_valid >= ROWS) {
 #pragma unroll
     for (int j = 0; j < INSTR; ++j) {
       const int J = wave * INSTR + j;
-      const char* s = src + (size_t)(J * kRpc) * stride;
-      dma_16(s + ((J & 1) ? plan.off[1] : plan.off[0]), lds + J * 1024);
+      const int Jb = J / BLOCK_COPIES, Ji = J % BLOCK_COPIES;
+      const char* s = src + (size_t)Jb * COL_STEP + (size_t)(Ji * kRpc) * stride;
+      const uint32_t lo = (INSTR % 2 == 0) ? ((j & 1) ? plan.off_odd : plan.off_even)
+                                           : (((wave * INSTR + j) & 1) ? plan.off_odd : plan.off_even);
+      dma_16(s, lo, lds + J * 1024);
     }
   } else {
 #pragma unroll
     for (int j = 0; j < INSTR; ++j) {
       const int J = wave * INSTR + j;
-      const int r = J * kRpc + plan.row_in_copy;
+      const int Jb = J / BLOCK_COPIES, Ji = J % BLOCK_COPIES;
+      const int r = Ji * kRpc + plan.row_in_copy;
       const int c = (lane % DmaPlan<ROW_BYTES>::kCpr) ^ swz_key<ROW_BYTES>(r);
       const int rs = min(r, rows_valid - 1);
-      dma_16(src + (size_t)rs * stride + c * 16, lds + J * 1024);
+      dma_16(src, (uint32_t)(Jb * COL_STEP + rs * stride + c * 16), lds + J * 1024);
     }
   }
 }
 
-// Per-lane LDS fragment offsets for a swizzled tile with ROW_BYTES-byte rows: the 16-byte
-// granule 2*s + hi of row lq (+32 per block) is at frag[s & 3] + 32*(s & ~3).
+// Per-lane LDS fragment offsets for a swizzled tile with ROW_BYTES-byte rows: logical
+// granule 2*s + hi of row lq (+32 rows per 32-key block) is at at(s).  With key(r) =
+// 2*x1 + x0 the stored granule is 2*(s ^ x1) + (hi ^ x0), so four registers cover s = 0..3
+// (s = 0..1 for 64-byte rows).
 template <int ROW_BYTES>
 struct FragOffsets {
   int o[4];
   __device__ __forceinline__ explicit FragOffsets(int lane) {
     const int lq = lane & 31, hi = lane >> 5;
-    if constexpr (ROW_BYTES >= 128) {
-      const int x1 = (lq >> 1) & 3;
+    const int key = swz_key<ROW_BYTES>(lq);
+    const int x0 = key & 1, x1 = key >> 1;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) o[u] = lq * ROW_BYTES + 16 * (hi ^ (lq & 1)) + 32 * (u ^ x1);
-    } else {
-      const int y = (lq >> 1) & 3;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) o[u] = lq * ROW_BYTES + 16 * (hi ^ (y & 1)) + 32 * ((u & 1) ^ (y >> 1));
-    }
+    for (int u = 0; u < 4; ++u) o[u] = lq * ROW_BYTES + 16 * (hi ^ x0) + 32 * (u ^ x1);
   }
-  __device__ __forceinline__ int at(int s) const { return o[s & 3] + 32 * (s & ~3); }
+  __device__ __forceinline__ int at(int s) const { return o[s]; }
 };
 
 // S^T tile (64 keys x 32 queries of this wave) by the INT8 route: exact INT32 products.
@@ -151,16 +162,18 @@ __device__ __forceinline__ void qk_int8(const char* kst, const FragOffsets<D>& f
   }
 }
 
-// S^T tile by the FP16 route: FP16 products, FP32 accumulation.
+// S^T tile by the FP16 route: FP16 products, FP32 accumulation.  Channel half h of the key
+// tile (channels 64h .. 64h + 63) sits kKHalfBytes * h into the slot.
 template <int D>
-__device__ __forceinline__ void qk_fp16(const char* kst, const FragOffsets<2 * D>& fo,
+__device__ __forceinline__ void qk_fp16(const char* kst, const FragOffsets<128>& fo,
                                         const half8 (&qf)[D / 16], f32x16& acc0, f32x16& acc1) {
   acc0 = f32x16{};
   acc1 = f32x16{};
 #pragma unroll
   for (int s = 0; s < D / 16; ++s) {
-    const half8 a0 = as_half8(ld_lds_16(kst, fo.at(s)));
-    const half8 a1 = as_half8(ld_lds_16(kst, fo.at(s) + 32 * 2 * D));
+    const int off = fo.at(s & 3) + (s >> 2) * (kBlockN * 128);
+    const half8 a0 = as_half8(ld_lds_16(kst, off));
+    const half8 a1 = as_half8(ld_lds_16(kst, off + 32 * 128));
     acc0 = mfma_f16(a0, qf[s], acc0);
     acc1 = mfma_f16(a1, qf[s], acc1);
   }
@@ -225,12 +238,15 @@ __device__ __forceinline__ void softmax_step(float (&sv)[32], float c, int key0,
   z_run += zs;
 }
 
-// Map a linear workgroup id to (b, h_q, m): rows longest first (largest m first for causal
-// attention); when the number of KV streams (b, h_k) is a multiple of 8, workgroups that
-// share an XCD (id % 8) walk the same KV streams, so their K/V tiles meet in one L2.
+// Map a linear workgroup id to (b, first query head, m).  A workgroup serves HEADS query heads
+// of one GQA group (they share the KV head and its routing words).  Rows go longest first
+// (largest m first for causal attention); when the number of KV streams (b, h_k) is a multiple
+// of 8, workgroups that share an XCD (id % 8) walk the same KV streams, so their K/V tiles
+// meet in one L2.
+template <int HEADS>
 __device__ __forceinline__ void decode_unit(int id, int B, int Hq, int Hk, int T_m, int& b,
-                                            int& hq, int& hk, int& m) {
-  const int G = Hq / Hk;
+                                            int& hq0, int& hk, int& m) {
+  const int G = Hq / Hk / HEADS;   // workgroups per (KV stream, m)
   const int P = B * Hk;
   int m_rev, p, qg;
   if ((P & 7) == 0) {
@@ -250,7 +266,24 @@ __device__ __forceinline__ void decode_unit(int id, int B, int Hq, int Hk, int T
   m = T_m - 1 - m_rev;
   b = p / Hk;
   hk = p - b * Hk;
-  hq = hk * G + qg;
+  hq0 = hk * (Hq / Hk) + qg * HEADS;
+}
+
+// s_waitcnt takes an immediate: wait until at most `n` vector-memory operations of this wave
+// are outstanding (loads complete in issue order).  `n` is wave-uniform.
+__device__ __forceinline__ void wait_vmem_at_most(int n) {
+  switch (n) {
+#define TM_WAIT_CASE(k) case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
+    TM_WAIT_CASE(0) TM_WAIT_CASE(1) TM_WAIT_CASE(2) TM_WAIT_CASE(3) TM_WAIT_CASE(4)
+    TM_WAIT_CASE(5) TM_WAIT_CASE(6) TM_WAIT_CASE(7) TM_WAIT_CASE(8) TM_WAIT_CASE(9)
+    TM_WAIT_CASE(10) TM_WAIT_CASE(11) TM_WAIT_CASE(12) TM_WAIT_CASE(13) TM_WAIT_CASE(14)
+    TM_WAIT_CASE(15) TM_WAIT_CASE(16) TM_WAIT_CASE(17) TM_WAIT_CASE(18) TM_WAIT_CASE(19)
+    TM_WAIT_CASE(20) TM_WAIT_CASE(21) TM_WAIT_CASE(22) TM_WAIT_CASE(23) TM_WAIT_CASE(24)
+    TM_WAIT_CASE(25) TM_WAIT_CASE(26) TM_WAIT_CASE(27) TM_WAIT_CASE(28) TM_WAIT_CASE(29)
+    TM_WAIT_CASE(30) TM_WAIT_CASE(31) TM_WAIT_CASE(32)
+#undef TM_WAIT_CASE
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
 }
 
 __device__ __forceinline__ float load_scale_uniform(const uint16_t* base, size_t idx) {
@@ -260,19 +293,22 @@ __device__ __forceinline__ float load_scale_uniform(const uint16_t* base, size_t
   return half_bits_to_float((uint16_t)((idx & 1) ? (w >> 16) : (w & 0xffffu)));
 }
 
-template <int D, int BM>
-__global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) {
-  using C = TileCfg<D, BM>;
-  __shared__ __align__(16) char smem[2 * C::kStage];
+template <int D, int BM, int HEADS, int NSTAGE>
+__global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) {
+  using C = TileCfg<D, BM, HEADS>;
+  __shared__ __align__(16) char smem[NSTAGE * C::kStage];
+  __shared__ uint16_t key_scale[kMaxKeyTiles];   // dK of this row's key tiles (FP16 bits)
 
-  int b, hq, hk, m;
-  decode_unit(blockIdx.x, a.B, a.Hq, a.Hk, a.T_m, b, hq, hk, m);
+  int b, hq0, hk, m;
+  decode_unit<HEADS>(blockIdx.x, a.B, a.Hq, a.Hk, a.T_m, b, hq0, hk, m);
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int hq = hq0 + wave / C::kWavesPerHead;   // this wave's query head
+  const int wave_in_head = wave % C::kWavesPerHead;
   const int lane = tid & (kWave - 1);
   const int lq = lane & 31, hi = lane >> 5;
-  const int q0 = m * BM + 32 * wave;          // first query row of this wave
+  const int q0 = m * BM + 32 * wave_in_head;  // first query row of this wave
   const int my_q = q0 + lq;
   // Row i may see keys j <= i + off (bottom-right causal alignment); without the causal
   // mask every key up to L_k - 1 is legal.
@@ -295,25 +331,28 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
   }
   const int n_end = wg_last_key / kBlockN;
 
+  // Routing words of this row: lane w holds word w (at most 64 words per row), so the
+  // per-tile lookup is a lane read plus a shift-and-mask, with no memory access in the loop.
   const uint64_t* route_row =
       a.route + (size_t)b * a.route_batch_stride + ((size_t)hk * a.T_m + m) * a.W;
+  const uint64_t my_word = (!a.force_fp16 && lane < a.W) ? route_row[lane] : 0ull;
+  const uint32_t word_lo = (uint32_t)my_word, word_hi = (uint32_t)(my_word >> 32);
   auto route_of = [&](int n) -> bool {
-    if (a.force_fp16) return false;
     const int gj = n / a.g;
-    return (route_row[gj >> 6] >> (gj & 63)) & 1ull;
+    const int w = gj >> 6, bit = gj & 63;
+    const uint32_t half = bit < 32 ? __builtin_amdgcn_readlane(word_lo, w)
+                                   : __builtin_amdgcn_readlane(word_hi, w);
+    return (half >> (bit & 31)) & 1u;
   };
 
   // Which operand forms this row needs (looked up once per row).
   bool need_int8 = false, need_fp16 = false;
   {
     const int g_last = n_end / a.g;
-    for (int w = 0; w <= (g_last >> 6); ++w) {
-      const int nb = min(64, g_last - 64 * w + 1);
-      const uint64_t valid = (nb >= 64) ? ~0ull : ((1ull << nb) - 1ull);
-      const uint64_t word = a.force_fp16 ? 0ull : route_row[w];
-      need_int8 |= (word & valid) != 0ull;
-      need_fp16 |= (~word & valid) != 0ull;
-    }
+    const int nb = g_last - 64 * lane + 1;      // groups of the row in this lane's word
+    const uint64_t valid = nb <= 0 ? 0ull : (nb >= 64 ? ~0ull : ((1ull << nb) - 1ull));
+    need_int8 = __any((my_word & valid) != 0ull);
+    need_fp16 = __any((~my_word & valid) != 0ull);
   }
 
   // Q operands of this wave, kept in registers for the whole row.
@@ -332,6 +371,10 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
                        : 0.0f;
   const float c_fp16 = a.scale_log2e;
   const float c_int8_q = a.scale_log2e * dq;
+  if (need_int8) {   // key-block scales of the tiles this row visits (key block = key tile)
+    for (int t = tid; t <= n_end; t += C::kThreads)
+      key_scale[t] = a.dK[((size_t)b * a.nKB + t) * a.Hk + hk];
+  }
 
   // Tile sources (uniform bases) and per-lane LDS fragment offsets.
   const int kstride = a.Hk * D * 2;                              // bytes between keys (FP16)
@@ -342,21 +385,23 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
   const DmaPlan<C::kKRow> plan_k(lane, kstride);
   const DmaPlan<C::kK8Row> plan_k8(lane, kstride / 2);
   const DmaPlan<C::kVRow> plan_v(lane, C::kVRow);
-  auto issue = [&](int n, bool int8) {   // start copying key tile n into stage n & 1
-    char* st = smem + (n & 1) * C::kStage;
+  auto stage_of = [&](int n) -> char* { return smem + (n % NSTAGE) * C::kStage; };
+  const uint32_t smem_lds = lds_addr_of(smem);
+  auto copies = [&](bool int8) -> int { return (int8 ? C::kK8Instr : C::kKInstr) + C::kVInstr; };
+  auto issue = [&](int n, bool int8) {   // start copying key tile n into its stage
+    const uint32_t st = smem_lds + (uint32_t)((n % NSTAGE) * C::kStage);
     const int rows = min(kBlockN, a.Lk - n * kBlockN);
     if (int8)
       dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(k8base + (size_t)n * kBlockN * (kstride / 2),
                                                 kstride / 2, rows, st, wave, lane, plan_k8);
-    else
-      dma_tile<C::kKRow, C::kKInstr, kBlockN>(kbase + (size_t)n * kBlockN * kstride, kstride, rows,
-                                              st, wave, lane, plan_k);
+    else   // 8 copies per 64-channel half of the FP16 key tile
+      dma_tile<C::kKRow, C::kKInstr, kBlockN, 8, 128>(kbase + (size_t)n * kBlockN * kstride, kstride,
+                                                      rows, st, wave, lane, plan_k);
     dma_tile<C::kVRow, C::kVInstr, D>(vbase + (size_t)n * (D * kBlockN * 2), C::kVRow, D,
                                       st + C::kKBytes, wave, lane, plan_v);
   };
-  const FragOffsets<C::kKRow> fo_k(lane);
+  const FragOffsets<128> fo_128(lane);      // K (FP16 halves), V^T, and K8 when d = 128
   const FragOffsets<C::kK8Row> fo_k8(lane);
-  const FragOffsets<C::kVRow> fo_v(lane);
 
   // Online-softmax state (Section 3.1), FP32; max kept in log2 units.
   float m_run = kNegInf;
@@ -365,25 +410,23 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
 #pragma unroll
   for (int c = 0; c < D / 32; ++c) oacc[c] = f32x16{};
 
-  bool r_cur = route_of(0);
-  issue(0, r_cur);
-  wait_vmem();
+  // Copies run NSTAGE - 1 tiles ahead of the math.
+  for (int t = 0; t < NSTAGE - 1; ++t)
+    if (t <= n_end) issue(t, route_of(t));
+  wait_all_memory();
   __syncthreads();
 
-  // One key tile: prefetch tile n + 1, compute tile n, publish the prefetch.  MASKED tiles
-  // apply the causal / sequence-end mask; they are the tiles past the first key tile that
-  // some row of the workgroup cannot fully see, and run in a loop of their own so the
-  // unmasked loop stays lean.
+  // One key tile: start copying tile n + NSTAGE - 1, compute tile n, then make sure tile n + 1
+  // has landed for every wave.  MASKED tiles apply the causal / sequence-end mask; they are
+  // the tiles past the first key tile that some row of the workgroup cannot fully see, and
+  // run in a loop of their own so the unmasked loop stays lean.
   auto step = [&](int n, auto masked_tag) {
     constexpr bool kMasked = decltype(masked_tag)::value;
-    const char* kst = smem + (n & 1) * C::kStage;
+    const bool r_cur = route_of(n);
+    const char* kst = stage_of(n);
     const char* vst = kst + C::kKBytes;
-    const bool has_next = n < n_end;
-    bool r_next = false;
-    if (has_next) {
-      r_next = route_of(n + 1);
-      issue(n + 1, r_next);
-    }
+    const int nf = n + NSTAGE - 1;
+    if (nf <= n_end) issue(nf, route_of(nf));
     const int key0 = n * kBlockN;
     if (wave_active && (!kMasked || key0 <= wave_last_key)) {
       float sv[32];
@@ -396,10 +439,10 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
           sv[r] = (float)i0[r];
           sv[16 + r] = (float)i1[r];
         }
-        c = c_int8_q * load_scale_uniform(a.dK, ((size_t)b * a.nKB + n) * a.Hk + hk);
+        c = c_int8_q * half_bits_to_float(key_scale[n]);
       } else {
         f32x16 f0, f1;
-        qk_fp16<D>(kst, fo_k, qf, f0, f1);
+        qk_fp16<D>(kst, fo_128, qf, f0, f1);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           sv[r] = f0[r];
@@ -415,14 +458,16 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
       for (int t = 0; t < 4; ++t) {
 #pragma unroll
         for (int cc = 0; cc < D / 32; ++cc) {
-          const half8 va = as_half8(ld_lds_16(vst, fo_v.at(t) + cc * 32 * C::kVRow));
+          const half8 va = as_half8(ld_lds_16(vst, fo_128.at(t) + cc * 32 * C::kVRow));
           oacc[cc] = mfma_f16(va, pfr[t], oacc[cc]);
         }
       }
     }
-    wait_vmem();       // the copies of tile n + 1 have landed in LDS
-    __syncthreads();   // ... for every wave, and every wave is done reading tile n
-    r_cur = r_next;
+    // Copies of tiles n + 2 .. nf may stay in flight; tile n + 1 must have landed.
+    int pending = 0;
+    for (int t = n + 2; t <= min(nf, n_end); ++t) pending += copies(route_of(t));
+    wait_vmem_at_most(pending);
+    __syncthreads();   // tile n + 1 visible to every wave; every wave is done reading tile n
   };
 
   // Tiles whose every key every row of the workgroup may see: keys <= the first row's last key.
@@ -455,7 +500,7 @@ __global__ __launch_bounds__(2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) 
 // INT8 route of the fused kernel.  One workgroup per requested tile.
 template <int D, int BM>
 __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
-  using C = TileCfg<D, BM>;
+  using C = TileCfg<D, BM, 1>;
   __shared__ __align__(16) char smem[C::kStage];
   const int e = blockIdx.x;
   const int b = a.tiles[4 * e + 0], hq = a.tiles[4 * e + 1];
@@ -477,8 +522,9 @@ __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
                     ((size_t)b * a.Lk * a.Hk + hk) * D + (size_t)n * kBlockN * (kstride / 2);
   const int rows = min(kBlockN, a.Lk - n * kBlockN);
   const DmaPlan<C::kK8Row> plan_k8(lane, kstride / 2);
-  dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(k8t, kstride / 2, rows, smem, wave, lane, plan_k8);
-  wait_vmem();
+  dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(k8t, kstride / 2, rows, lds_addr_of(smem), wave, lane,
+                                            plan_k8);
+  wait_all_memory();
   __syncthreads();
   const int my_q = m * BM + 32 * wave + lq;
   i32x4 q8f[D / 32];
@@ -498,19 +544,19 @@ __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
   }
 }
 
-template <int D, int BM>
+template <int D, int BM, int HEADS, int NSTAGE>
 hipError_t launch_attn_t(const AttnArgs& a, hipStream_t stream) {
-  using C = TileCfg<D, BM>;
-  const long long grid = (long long)a.B * a.Hq * a.T_m;
+  using C = TileCfg<D, BM, HEADS>;
+  const long long grid = (long long)a.B * (a.Hq / HEADS) * a.T_m;
   if (grid <= 0 || grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM>), dim3((unsigned)grid), dim3(C::kThreads), 0,
-                     stream, a);
+  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS, NSTAGE>), dim3((unsigned)grid),
+                     dim3(C::kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
 template <int D, int BM>
 hipError_t launch_debug_t(const DebugTileArgs& a, hipStream_t stream) {
-  using C = TileCfg<D, BM>;
+  using C = TileCfg<D, BM, 1>;
   hipLaunchKernelGGL((debug_tiles_kernel<D, BM>), dim3(a.count), dim3(C::kThreads), 0, stream, a);
   return hipGetLastError();
 }
@@ -518,10 +564,15 @@ hipError_t launch_debug_t(const DebugTileArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_routed_attention(const AttnArgs& a, int d, int block_m, hipStream_t stream) {
-  if (d == 128 && block_m == 128) return launch_attn_t<128, 128>(a, stream);
-  if (d == 128 && block_m == 64) return launch_attn_t<128, 64>(a, stream);
-  if (d == 64 && block_m == 128) return launch_attn_t<64, 128>(a, stream);
-  if (d == 64 && block_m == 64) return launch_attn_t<64, 64>(a, stream);
+  // d = 128: two query heads of a GQA group per workgroup (one K/V copy serves both) when the
+  // group has an even number of heads, with three LDS stages.  d = 64: one head, four stages.
+  const bool pair = ((a.Hq / a.Hk) % 2) == 0;
+  if (d == 128 && block_m == 128)
+    return pair ? launch_attn_t<128, 128, 2, 3>(a, stream) : launch_attn_t<128, 128, 1, 2>(a, stream);
+  if (d == 128 && block_m == 64)
+    return pair ? launch_attn_t<128, 64, 2, 2>(a, stream) : launch_attn_t<128, 64, 1, 2>(a, stream);
+  if (d == 64 && block_m == 128) return launch_attn_t<64, 128, 1, 4>(a, stream);
+  if (d == 64 && block_m == 64) return launch_attn_t<64, 64, 1, 4>(a, stream);
   return hipErrorInvalidValue;
 }
 

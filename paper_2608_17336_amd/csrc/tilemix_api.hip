@@ -64,6 +64,9 @@ tilemix_status validate(const tilemix_params* p) {
   const long long rows_k = (long long)p->batch * p->len_k * p->heads_kv;
   if (rows_q * p->head_dim > (1LL << 40) || rows_k * p->head_dim > (1LL << 40))
     return fail(TILEMIX_ERR_SHAPE, "tensor too large");
+  if (cdiv(p->len_k, p->block_n) > tilemix::kMaxKeyTiles)
+    return fail(TILEMIX_ERR_UNSUPPORTED, "len_k %d exceeds the supported %d keys", p->len_k,
+                tilemix::kMaxKeyTiles * tilemix::kBlockN);
   const long long grid = (long long)p->batch * p->heads_q * cdiv(p->len_q, p->block_m);
   if (grid > 0x7fffffffLL) return fail(TILEMIX_ERR_SHAPE, "too many query tiles");
   if ((long long)p->heads_kv * p->batch > 65535 || p->heads_q > 65535)

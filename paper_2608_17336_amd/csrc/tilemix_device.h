@@ -24,6 +24,9 @@ constexpr int kWave = 64;
 constexpr int kQuantBlockQ = 128;  // query rows per INT8 scale block (Appendix C)
 constexpr int kQuantBlockK = 64;   // key rows per INT8 scale block (Appendix C)
 constexpr int kBlockN = 64;        // keys per compute tile (= key scale block)
+constexpr int kMaxKeyTiles = 4096; // key tiles per row whose scales the kernel holds in LDS
+                                   // (L_k <= 262144); also bounds the routing words per row
+                                   // to 64, which one register pair per wave holds
 
 __device__ __forceinline__ float half_bits_to_float(uint16_t h) {
   _Float16 v;
@@ -46,17 +49,27 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __builtin_bit_cast(float, (int)r[0]) + __builtin_bit_cast(float, (int)r[1]);
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void global_void_t;
-
-// Direct global -> LDS copy of 16 bytes per lane: lane l of the wave writes
-// lds_wave_base + 16*l (lds_wave_base must be wave-uniform).  Completion is tracked by
-// vmcnt like any vector load.
-__device__ __forceinline__ void dma_16(const void* src, char* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds((global_void_t*)src, (lds_void_t*)lds_wave_base, 16, 0, 0);
+// Direct global -> LDS copy of 16 bytes per lane: lane l reads base + voff and writes LDS byte
+// lds_addr + 16*l (base and lds_addr wave-uniform).  Completion is tracked by vmcnt like any
+// vector load; it is issued as inline assembly so that the only waits on it are the explicit
+// vmcnt waits of the caller (the compiler would otherwise wait for every copy in flight
+// before any LDS read, whichever LDS bytes the copies write).
+__device__ __forceinline__ void dma_16(const void* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_addr)
+               : "m0");
 }
 
-__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// 32-bit LDS address of a __shared__ object.
+template <typename T>
+__device__ __forceinline__ uint32_t lds_addr_of(T* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(p);
+}
+
+// Wait for every outstanding memory operation of the wave (vector, scalar, LDS).  Emitted with
+// the builtin, so the compiler knows its own earlier loads are complete as well.
+__device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
 
 __device__ __forceinline__ uint4 ld_global_16(const void* p) {
   return *reinterpret_cast<const uint4*>(p);
