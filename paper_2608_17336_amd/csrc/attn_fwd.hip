@@ -293,7 +293,7 @@ __device__ __forceinline__ float load_scale_uniform(const uint16_t* base, size_t
   return half_bits_to_float((uint16_t)((idx & 1) ? (w >> 16) : (w & 0xffffu)));
 }
 
-template <int D, int BM, int HEADS, int NSTAGE>
+template <int D, int BM, int HEADS, int NSTAGE, bool PINGPONG>
 __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) {
   using C = TileCfg<D, BM, HEADS>;
   __shared__ __align__(16) char smem[NSTAGE * C::kStage];
@@ -410,72 +410,130 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
 #pragma unroll
   for (int c = 0; c < D / 32; ++c) oacc[c] = f32x16{};
 
-  // Copies run NSTAGE - 1 tiles ahead of the math.
-  for (int t = 0; t < NSTAGE - 1; ++t)
+  // Raw scores of key tile n for this wave (INT32 products converted to float, or FP32 dot
+  // products) and the factor c that turns them into log2-domain scaled scores.
+  auto qk = [&](int n, float (&sv)[32], float& c) {
+    const char* kst = stage_of(n);
+    if (route_of(n)) {
+      i32x16 i0, i1;
+      qk_int8<D>(kst, fo_k8, q8f, i0, i1);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sv[r] = (float)i0[r];
+        sv[16 + r] = (float)i1[r];
+      }
+      c = c_int8_q * half_bits_to_float(key_scale[n]);
+    } else {
+      f32x16 f0, f1;
+      qk_fp16<D>(kst, fo_128, qf, f0, f1);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sv[r] = f0[r];
+        sv[16 + r] = f1[r];
+      }
+      c = c_fp16;
+    }
+  };
+  // O^T += V^T P^T for key tile n: granule 2t + hi of V^T row 32*cc + lq holds the keys of
+  // P^T slot t.
+  auto pv = [&](int n, const half8 (&pfr)[4]) {
+    const char* vst = stage_of(n) + C::kKBytes;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int cc = 0; cc < D / 32; ++cc) {
+        const half8 va = as_half8(ld_lds_16(vst, fo_128.at(t) + cc * 32 * C::kVRow));
+        oacc[cc] = mfma_f16(va, pfr[t], oacc[cc]);
+      }
+    }
+  };
+  // Does this wave have a legal key in tile n (only in doubt on masked tiles)?
+  auto sees = [&](int n, bool masked) { return wave_active && (!masked || n * kBlockN <= wave_last_key); };
+
+  // Schedule.  Copies run PD tiles ahead of the math.  With PINGPONG the second head of the
+  // pair runs each tile half an iteration late: while the first head's wave multiplies Q K^T of
+  // tile n on the matrix cores, its SIMD partner (same SIMD, other head) runs the softmax of
+  // tile n - 1 on the vector ALU, then takes the matrix cores for P.V of tile n - 1 and Q K^T of
+  // tile n while the first head runs its softmax.  It keeps tile n - 1's scores in registers
+  // across the tile barrier and needs V of tile n - 1 still resident: one extra LDS stage.
+  constexpr int PD = PINGPONG ? NSTAGE - 2 : NSTAGE - 1;
+  static_assert(PD >= 1, "at least one tile of copy lead");
+  static_assert(!PINGPONG || HEADS == 2, "ping-pong pairs the two heads of a workgroup");
+  const bool late = PINGPONG && (wave >= C::kWavesPerHead);
+
+  for (int t = 0; t < PD; ++t)
     if (t <= n_end) issue(t, route_of(t));
   wait_all_memory();
   __syncthreads();
 
-  // One key tile: start copying tile n + NSTAGE - 1, compute tile n, then make sure tile n + 1
-  // has landed for every wave.  MASKED tiles apply the causal / sequence-end mask; they are
-  // the tiles past the first key tile that some row of the workgroup cannot fully see, and
-  // run in a loop of their own so the unmasked loop stays lean.
-  auto step = [&](int n, auto masked_tag) {
-    constexpr bool kMasked = decltype(masked_tag)::value;
-    const bool r_cur = route_of(n);
-    const char* kst = stage_of(n);
-    const char* vst = kst + C::kKBytes;
-    const int nf = n + NSTAGE - 1;
-    if (nf <= n_end) issue(nf, route_of(nf));
-    const int key0 = n * kBlockN;
-    if (wave_active && (!kMasked || key0 <= wave_last_key)) {
-      float sv[32];
-      float c;   // factor from raw score to log2-domain scaled score
-      if (r_cur) {
-        i32x16 i0, i1;
-        qk_int8<D>(kst, fo_k8, q8f, i0, i1);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          sv[r] = (float)i0[r];
-          sv[16 + r] = (float)i1[r];
-        }
-        c = c_int8_q * half_bits_to_float(key_scale[n]);
-      } else {
-        f32x16 f0, f1;
-        qk_fp16<D>(kst, fo_128, qf, f0, f1);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          sv[r] = f0[r];
-          sv[16 + r] = f1[r];
-        }
-        c = c_fp16;
-      }
-      half8 pfr[4];
-      softmax_step<D, kMasked>(sv, c, key0, my_last_key, lane, m_run, z_run, oacc, pfr);
-
-      // O^T += V^T P^T: granule 2t + hi of V^T row 32*cc + lq holds the keys of P^T slot t.
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-#pragma unroll
-        for (int cc = 0; cc < D / 32; ++cc) {
-          const half8 va = as_half8(ld_lds_16(vst, fo_128.at(t) + cc * 32 * C::kVRow));
-          oacc[cc] = mfma_f16(va, pfr[t], oacc[cc]);
-        }
-      }
-    }
-    // Copies of tiles n + 2 .. nf may stay in flight; tile n + 1 must have landed.
+  // Start the copy of tile n + PD; at the end of a tile, tile n + 1 must have landed for every
+  // wave while copies of tiles n + 2 .. n + PD may stay in flight.
+  auto prefetch = [&](int n) {
+    if (n + PD <= n_end) issue(n + PD, route_of(n + PD));
+  };
+  auto finish_tile = [&](int n) {
     int pending = 0;
-    for (int t = n + 2; t <= min(nf, n_end); ++t) pending += copies(route_of(t));
+    for (int t = n + 2; t <= min(n + PD, n_end); ++t) pending += copies(route_of(t));
     wait_vmem_at_most(pending);
-    __syncthreads();   // tile n + 1 visible to every wave; every wave is done reading tile n
+    __syncthreads();   // tile n + 1 visible to every wave; the oldest stage released
+  };
+  auto early_tile = [&](int n, auto masked_tag) {
+    constexpr bool kMasked = decltype(masked_tag)::value;
+    prefetch(n);
+    if (sees(n, kMasked)) {
+      float sv[32], c;
+      qk(n, sv, c);
+      half8 pfr[4];
+      softmax_step<D, kMasked>(sv, c, n * kBlockN, my_last_key, lane, m_run, z_run, oacc, pfr);
+      pv(n, pfr);
+    }
+    finish_tile(n);
   };
 
   // Tiles whose every key every row of the workgroup may see: keys <= the first row's last key.
   const int wg_first_row_last_key = min(a.Lk - 1, m * BM + off);
   const int n_split = max(0, min(n_end + 1, (wg_first_row_last_key + 1) / kBlockN));
-  int n = 0;
-  for (; n < n_split; ++n) step(n, std::integral_constant<bool, false>{});
-  for (; n <= n_end; ++n) step(n, std::integral_constant<bool, true>{});
+  using Unmasked = std::integral_constant<bool, false>;
+  using Masked = std::integral_constant<bool, true>;
+  if (!late) {
+    int n = 0;
+    for (; n < n_split; ++n) early_tile(n, Unmasked{});
+    for (; n <= n_end; ++n) early_tile(n, Masked{});
+  } else {
+    float sv_late[32];   // scores of the previous tile, carried across the tile barrier
+    float c_late = 0.0f;
+    // Each tile's softmax uses the same (masked or unmasked) variant as in the early head, so
+    // the two heads compute bit-identical results on identical inputs.
+    auto late_tile = [&](int n, auto prev_masked_tag, auto cur_masked_tag) {
+      constexpr bool kPrevMasked = decltype(prev_masked_tag)::value;
+      constexpr bool kCurMasked = decltype(cur_masked_tag)::value;
+      prefetch(n);
+      if (n >= 1 && sees(n - 1, kPrevMasked)) {
+        half8 pfr[4];
+        softmax_step<D, kPrevMasked>(sv_late, c_late, (n - 1) * kBlockN, my_last_key, lane, m_run,
+                                     z_run, oacc, pfr);
+        pv(n - 1, pfr);
+      }
+      if (sees(n, kCurMasked)) qk(n, sv_late, c_late);
+      finish_tile(n);
+    };
+    int n = 0;
+    for (; n < n_split; ++n) late_tile(n, Unmasked{}, Unmasked{});
+    if (n <= n_end) late_tile(n++, Unmasked{}, Masked{});
+    for (; n <= n_end; ++n) late_tile(n, Masked{}, Masked{});
+    half8 pfr[4];   // the last tile's softmax and P.V
+    if (n_end < n_split) {
+      if (sees(n_end, false)) {
+        softmax_step<D, false>(sv_late, c_late, n_end * kBlockN, my_last_key, lane, m_run, z_run,
+                               oacc, pfr);
+        pv(n_end, pfr);
+      }
+    } else if (sees(n_end, true)) {
+      softmax_step<D, true>(sv_late, c_late, n_end * kBlockN, my_last_key, lane, m_run, z_run,
+                            oacc, pfr);
+      pv(n_end, pfr);
+    }
+  }
 
   // Epilogue: O = O~ / z~, FP16 (round to nearest even).
   if (wave_active) {
@@ -544,12 +602,12 @@ __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
   }
 }
 
-template <int D, int BM, int HEADS, int NSTAGE>
+template <int D, int BM, int HEADS, int NSTAGE, bool PINGPONG = false>
 hipError_t launch_attn_t(const AttnArgs& a, hipStream_t stream) {
   using C = TileCfg<D, BM, HEADS>;
   const long long grid = (long long)a.B * (a.Hq / HEADS) * a.T_m;
   if (grid <= 0 || grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS, NSTAGE>), dim3((unsigned)grid),
+  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS, NSTAGE, PINGPONG>), dim3((unsigned)grid),
                      dim3(C::kThreads), 0, stream, a);
   return hipGetLastError();
 }
@@ -568,7 +626,7 @@ hipError_t launch_routed_attention(const AttnArgs& a, int d, int block_m, hipStr
   // group has an even number of heads, with three LDS stages.  d = 64: one head, four stages.
   const bool pair = ((a.Hq / a.Hk) % 2) == 0;
   if (d == 128 && block_m == 128)
-    return pair ? launch_attn_t<128, 128, 2, 3>(a, stream) : launch_attn_t<128, 128, 1, 2>(a, stream);
+    return pair ? launch_attn_t<128, 128, 2, 3, true>(a, stream) : launch_attn_t<128, 128, 1, 2>(a, stream);
   if (d == 128 && block_m == 64)
     return pair ? launch_attn_t<128, 64, 2, 2>(a, stream) : launch_attn_t<128, 64, 1, 2>(a, stream);
   if (d == 64 && block_m == 128) return launch_attn_t<64, 128, 1, 4>(a, stream);
