@@ -37,9 +37,23 @@
 #include "tilemix_device.h"
 #include "tilemix_internal.h"
 
+#ifndef TM_HEADS
+#define TM_HEADS 1
+#endif
+
 namespace tilemix {
 
 namespace {
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I = B .. E - 1, so every index the
+// body derives from I is a constant (registers are never indexed dynamically).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 constexpr float kRescaleThreshold = 8.0f;   // log2 units: rescale when the max grows > x256
 constexpr float kNegInf = -__builtin_huge_valf();
@@ -269,23 +283,6 @@ __device__ __forceinline__ void decode_unit(int id, int B, int Hq, int Hk, int T
   hq0 = hk * (Hq / Hk) + qg * HEADS;
 }
 
-// s_waitcnt takes an immediate: wait until at most `n` vector-memory operations of this wave
-// are outstanding (loads complete in issue order).  `n` is wave-uniform.
-__device__ __forceinline__ void wait_vmem_at_most(int n) {
-  switch (n) {
-#define TM_WAIT_CASE(k) case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
-    TM_WAIT_CASE(0) TM_WAIT_CASE(1) TM_WAIT_CASE(2) TM_WAIT_CASE(3) TM_WAIT_CASE(4)
-    TM_WAIT_CASE(5) TM_WAIT_CASE(6) TM_WAIT_CASE(7) TM_WAIT_CASE(8) TM_WAIT_CASE(9)
-    TM_WAIT_CASE(10) TM_WAIT_CASE(11) TM_WAIT_CASE(12) TM_WAIT_CASE(13) TM_WAIT_CASE(14)
-    TM_WAIT_CASE(15) TM_WAIT_CASE(16) TM_WAIT_CASE(17) TM_WAIT_CASE(18) TM_WAIT_CASE(19)
-    TM_WAIT_CASE(20) TM_WAIT_CASE(21) TM_WAIT_CASE(22) TM_WAIT_CASE(23) TM_WAIT_CASE(24)
-    TM_WAIT_CASE(25) TM_WAIT_CASE(26) TM_WAIT_CASE(27) TM_WAIT_CASE(28) TM_WAIT_CASE(29)
-    TM_WAIT_CASE(30) TM_WAIT_CASE(31) TM_WAIT_CASE(32)
-#undef TM_WAIT_CASE
-    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-  }
-}
-
 __device__ __forceinline__ float load_scale_uniform(const uint16_t* base, size_t idx) {
   // The scale arrays live in 256-byte aligned workspace slots, so reading the aligned
   // 32-bit word that holds element idx stays inside the slot.
@@ -293,10 +290,47 @@ __device__ __forceinline__ float load_scale_uniform(const uint16_t* base, size_t
   return half_bits_to_float((uint16_t)((idx & 1) ? (w >> 16) : (w & 0xffffu)));
 }
 
-template <int D, int BM, int HEADS, int NSTAGE, bool PINGPONG>
+// max(a, b, c) in one instruction.  The scores are never NaN, so the operand quieting that a
+// library max would add is not needed.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Exp half of the online-softmax step for score pair J of a lane (elements i, i + 1 of its 32
+// scores, held in two accumulator blocks, taken in P.V operand order): P = 2^(c*s - msub) rounded to FP16 into its operand
+// slot, and the FP16 pair added to the row-sum partial, so the normalizer sums exactly the P
+// that P.V multiplies.
+template <int J>
+__device__ __forceinline__ void exp_pair(const f32x16& x0, const f32x16& x1, float c, float msub,
+                                         half8 (&pfr)[4], float& zs) {
+  constexpr int t = J >> 2, e = 2 * (J & 3);
+  constexpr int i = 16 * (t >> 1) + 8 * (t & 1) + e;
+  float s0, s1;
+  if constexpr (i < 16) {
+    s0 = x0[i];
+    s1 = x0[i + 1];
+  } else {
+    s0 = x1[i - 16];
+    s1 = x1[i - 15];
+  }
+  const float p0 = __builtin_amdgcn_exp2f(fmaf(s0, c, -msub));
+  const float p1 = __builtin_amdgcn_exp2f(fmaf(s1, c, -msub));
+  const half2v pr = {(_Float16)p0, (_Float16)p1};
+  const half2v ones = {(_Float16)1.0f, (_Float16)1.0f};
+  zs = __builtin_amdgcn_fdot2(pr, ones, zs, false);
+  pfr[t][e] = pr[0];
+  pfr[t][e + 1] = pr[1];
+}
+
+template <int D, int BM, int HEADS>
 __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) {
   using C = TileCfg<D, BM, HEADS>;
-  __shared__ __align__(16) char smem[NSTAGE * C::kStage];
+  // Two K slots and two V slots: step n reads K of tile n + 1 and V of tile n while K of tile
+  // n + 2 and V of tile n + 1 are copied into the slots that step n - 1 released.  72 KB at
+  // d = 128, so two workgroups share a CU and each SIMD runs one wave of each.
+  __shared__ __align__(16) char smem[2 * C::kKBytes + 2 * C::kVBytes];
   __shared__ uint16_t key_scale[kMaxKeyTiles];   // dK of this row's key tiles (FP16 bits)
 
   int b, hq0, hk, m;
@@ -318,7 +352,6 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   // Last key any row of the workgroup / of this wave may see.
   const int wg_last_key = min(a.Lk - 1, min(a.Lq - 1, m * BM + BM - 1) + off);
   const int wave_last_key = min(a.Lk - 1, min(a.Lq - 1, q0 + 31) + off);
-  const int first_row_last_key = min(a.Lk - 1, q0 + off);    // smallest last key of the wave
   const int my_last_key = min(a.Lk - 1, my_q + off);
 
   _Float16* orow = a.O + (((size_t)b * a.Lq + my_q) * a.Hq + hq) * D;
@@ -337,8 +370,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
       a.route + (size_t)b * a.route_batch_stride + ((size_t)hk * a.T_m + m) * a.W;
   const uint64_t my_word = (!a.force_fp16 && lane < a.W) ? route_row[lane] : 0ull;
   const uint32_t word_lo = (uint32_t)my_word, word_hi = (uint32_t)(my_word >> 32);
-  auto route_of = [&](int n) -> bool {
-    const int gj = n / a.g;
+  auto group_route = [&](int gj) -> bool {   // routing bit of tile group gj
     const int w = gj >> 6, bit = gj & 63;
     const uint32_t half = bit < 32 ? __builtin_amdgcn_readlane(word_lo, w)
                                    : __builtin_amdgcn_readlane(word_hi, w);
@@ -385,35 +417,71 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   const DmaPlan<C::kKRow> plan_k(lane, kstride);
   const DmaPlan<C::kK8Row> plan_k8(lane, kstride / 2);
   const DmaPlan<C::kVRow> plan_v(lane, C::kVRow);
-  auto stage_of = [&](int n) -> char* { return smem + (n % NSTAGE) * C::kStage; };
+  auto k_slot = [](int n) { return (n & 1) * C::kKBytes; };                   // LDS offsets
+  auto v_slot = [](int n) { return 2 * C::kKBytes + (n & 1) * C::kVBytes; };
   const uint32_t smem_lds = lds_addr_of(smem);
-  auto copies = [&](bool int8) -> int { return (int8 ? C::kK8Instr : C::kKInstr) + C::kVInstr; };
-  auto issue = [&](int n, bool int8) {   // start copying key tile n into its stage
-    const uint32_t st = smem_lds + (uint32_t)((n % NSTAGE) * C::kStage);
-    const int rows = min(kBlockN, a.Lk - n * kBlockN);
+
+  // Copies are issued in tile order, K and V each on their own.  The issue state advances by
+  // additions only: the next tile, its routing group (tile = group * g + r) and its source
+  // addresses.  The route of every issued K tile is kept in a 64-bit ring (bit t mod 64),
+  // which the math reads back; at most two K tiles are ever in flight.
+  int iss_kt = 0, iss_vt = 0, iss_g = 0, iss_r = 0;
+  uint64_t route_ring = 0;
+  const char* iss_k = kbase;
+  const char* iss_k8 = k8base;
+  const char* iss_v = vbase;
+  auto issue_k_next = [&]() {
+    const bool int8 = group_route(iss_g);
+    const uint64_t bit = 1ull << (iss_kt & 63);
+    route_ring = int8 ? (route_ring | bit) : (route_ring & ~bit);
+    const uint32_t dst = smem_lds + (uint32_t)k_slot(iss_kt);
+    const int rows = min(kBlockN, a.Lk - iss_kt * kBlockN);
     if (int8)
-      dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(k8base + (size_t)n * kBlockN * (kstride / 2),
-                                                kstride / 2, rows, st, wave, lane, plan_k8);
+      dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(iss_k8, kstride / 2, rows, dst, wave, lane, plan_k8);
     else   // 8 copies per 64-channel half of the FP16 key tile
-      dma_tile<C::kKRow, C::kKInstr, kBlockN, 8, 128>(kbase + (size_t)n * kBlockN * kstride, kstride,
-                                                      rows, st, wave, lane, plan_k);
-    dma_tile<C::kVRow, C::kVInstr, D>(vbase + (size_t)n * (D * kBlockN * 2), C::kVRow, D,
-                                      st + C::kKBytes, wave, lane, plan_v);
+      dma_tile<C::kKRow, C::kKInstr, kBlockN, 8, 128>(iss_k, kstride, rows, dst, wave, lane, plan_k);
+    ++iss_kt;
+    if (++iss_r == a.g) {
+      iss_r = 0;
+      ++iss_g;
+    }
+    iss_k += (size_t)kBlockN * kstride;
+    iss_k8 += (size_t)kBlockN * (kstride / 2);
+  };
+  auto issue_v_next = [&]() {
+    dma_tile<C::kVRow, C::kVInstr, D>(iss_v, C::kVRow, D, smem_lds + (uint32_t)v_slot(iss_vt), wave,
+                                      lane, plan_v);
+    ++iss_vt;
+    iss_v += (size_t)D * kBlockN * 2;
+  };
+  auto issue = [&](int k_last, int v_last) {
+    for (const int l = min(k_last, n_end); iss_kt <= l;) issue_k_next();
+    for (const int l = min(v_last, n_end); iss_vt <= l;) issue_v_next();
+  };
+  auto route_of = [&](int n) -> bool { return (route_ring >> (n & 63)) & 1ull; };   // issued K n
+  // Every copy issued so far has landed for every wave, then K through k_last and V through
+  // v_last are issued.  Each call site issues exactly the tiles whose slots the barrier freed.
+  auto sync = [&](int k_last, int v_last) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    issue(k_last, v_last);
   };
   const FragOffsets<128> fo_128(lane);      // K (FP16 halves), V^T, and K8 when d = 128
   const FragOffsets<C::kK8Row> fo_k8(lane);
 
   // Online-softmax state (Section 3.1), FP32; max kept in log2 units.
   float m_run = kNegInf;
+  float msub = 0.0f;   // the max that P subtracts (0 while no score has been seen)
   float z_run = 0.0f;
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int c = 0; c < D / 32; ++c) oacc[c] = f32x16{};
 
-  // Raw scores of key tile n for this wave (INT32 products converted to float, or FP32 dot
-  // products) and the factor c that turns them into log2-domain scaled scores.
+  // ---- Straight per-tile path, used for tiles that cross the causal diagonal or the sequence
+  // end.  Raw scores of key tile n (INT32 products converted to float, or FP32 dot products)
+  // and the factor c that turns them into log2-domain scaled scores.
   auto qk = [&](int n, float (&sv)[32], float& c) {
-    const char* kst = stage_of(n);
+    const char* kst = smem + k_slot(n);
     if (route_of(n)) {
       i32x16 i0, i1;
       qk_int8<D>(kst, fo_k8, q8f, i0, i1);
@@ -437,7 +505,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   // O^T += V^T P^T for key tile n: granule 2t + hi of V^T row 32*cc + lq holds the keys of
   // P^T slot t.
   auto pv = [&](int n, const half8 (&pfr)[4]) {
-    const char* vst = stage_of(n) + C::kKBytes;
+    const char* vst = smem + v_slot(n);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
 #pragma unroll
@@ -447,91 +515,202 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
       }
     }
   };
-  // Does this wave have a legal key in tile n (only in doubt on masked tiles)?
-  auto sees = [&](int n, bool masked) { return wave_active && (!masked || n * kBlockN <= wave_last_key); };
 
-  // Schedule.  Copies run PD tiles ahead of the math.  With PINGPONG the second head of the
-  // pair runs each tile half an iteration late: while the first head's wave multiplies Q K^T of
-  // tile n on the matrix cores, its SIMD partner (same SIMD, other head) runs the softmax of
-  // tile n - 1 on the vector ALU, then takes the matrix cores for P.V of tile n - 1 and Q K^T of
-  // tile n while the first head runs its softmax.  It keeps tile n - 1's scores in registers
-  // across the tile barrier and needs V of tile n - 1 still resident: one extra LDS stage.
-  constexpr int PD = PINGPONG ? NSTAGE - 2 : NSTAGE - 1;
-  static_assert(PD >= 1, "at least one tile of copy lead");
-  static_assert(!PINGPONG || HEADS == 2, "ping-pong pairs the two heads of a workgroup");
-  const bool late = PINGPONG && (wave >= C::kWavesPerHead);
+  // ---- Software-pipelined path for the tiles every row of the workgroup sees in full.  Each
+  // step interleaves, in one wave, matrix-core work of one tile with vector work of another:
+  //   phase A: Q K^T of tile n + 1           | exp half of tile n's softmax (P(n), row sum)
+  //   phase B: O += V^T P^T of tile n (P.V)  | row max of tile n + 1's scores
+  // and the max update (with the rare lazy rescale) closes the step.  Every chunk below is one
+  // MFMA plus its share of the vector work, kept in program order by a scheduling barrier;
+  // LDS fragments are read kLead chunks ahead of the MFMA that consumes them.  A tile's 32
+  // scores per lane live in two accumulator blocks (elements 0-15, 16-31); two such buffers
+  // alternate between "scores of tile n" and "scores of tile n + 1" from step to step.
+  constexpr int kLead = 3;
+  float c_cur = 0.0f;
 
-  for (int t = 0; t < PD; ++t)
-    if (t <= n_end) issue(t, route_of(t));
-  wait_all_memory();
-  __syncthreads();
-
-  // Start the copy of tile n + PD; at the end of a tile, tile n + 1 must have landed for every
-  // wave while copies of tiles n + 2 .. n + PD may stay in flight.
-  auto prefetch = [&](int n) {
-    if (n + PD <= n_end) issue(n + PD, route_of(n + PD));
-  };
-  auto finish_tile = [&](int n) {
-    int pending = 0;
-    for (int t = n + 2; t <= min(n + PD, n_end); ++t) pending += copies(route_of(t));
-    wait_vmem_at_most(pending);
-    __syncthreads();   // tile n + 1 visible to every wave; the oldest stage released
-  };
-  auto early_tile = [&](int n, auto masked_tag) {
-    constexpr bool kMasked = decltype(masked_tag)::value;
-    prefetch(n);
-    if (sees(n, kMasked)) {
-      float sv[32], c;
-      qk(n, sv, c);
-      half8 pfr[4];
-      softmax_step<D, kMasked>(sv, c, n * kBlockN, my_last_key, lane, m_run, z_run, oacc, pfr);
-      pv(n, pfr);
+  // Phase A.  QK: 0 = none (exp half only), 1 = FP16 route, 2 = INT8 route for tile n + 1,
+  // whose scores go to y0 / y1 as floats (INT8 route: the exact INT32 products converted).
+  auto phase_a = [&](auto qk_tag, auto exp_tag, int k_off, const f32x16& x0, const f32x16& x1,
+                     f32x16& y0, f32x16& y1, half8 (&pfr)[4], float& zs) {
+    constexpr int kQK = decltype(qk_tag)::value;
+    constexpr bool kExp = decltype(exp_tag)::value;
+    constexpr int NQ = kQK == 0 ? 4 : (kQK == 2 ? 2 * (D / 32) : 2 * (D / 16));   // chunks
+    // Chunk j feeds accumulator h = j / (NQ/2) with K slice s = j % (NQ/2): y0 is complete
+    // half-way through, and (INT8 route) is converted to float under the MFMAs of y1.
+    const char* kst = smem + k_off;
+    uint4 kf[NQ];
+    auto kload = [&](auto jc) {
+      constexpr int j = decltype(jc)::value, s = j % (NQ / 2), h = j / (NQ / 2);
+      if constexpr (kQK == 2) kf[j] = ld_lds_16(kst, fo_k8.at(s) + h * 32 * D);
+      else kf[j] = ld_lds_16(kst, fo_128.at(s & 3) + (s >> 2) * (kBlockN * 128) + h * 32 * 128);
+    };
+    if constexpr (kQK != 0) {
+      static_for<0, (kLead < NQ ? kLead : NQ)>(kload);
+      y0 = f32x16{};
+      y1 = f32x16{};
     }
-    finish_tile(n);
+    // Every call site computes the same exp half of tile n; an opaque copy of its inputs keeps
+    // each copy inside its own branch, interleaved with that branch's MFMAs, instead of being
+    // merged ahead of the branch.
+    float c_x = c_cur, msub_x = msub;
+    asm volatile("" : "+v"(c_x), "+v"(msub_x));
+    auto to_float = [](f32x16& y, int r) {
+      const float raw = y[r];   // (bit-casting the element lvalue itself reads element 0)
+      y[r] = (float)__builtin_bit_cast(int, raw);
+    };
+    float zs0 = 0.0f, zs1 = 0.0f;
+    static_for<0, NQ>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      if constexpr (kQK != 0) {
+        if constexpr (j + kLead < NQ) kload(std::integral_constant<int, j + kLead>{});
+        constexpr int s = j % (NQ / 2);
+        f32x16& acc = (j < NQ / 2) ? y0 : y1;
+        if constexpr (kQK == 2)
+          acc = __builtin_bit_cast(
+              f32x16, mfma_i8(as_i32x4(kf[j]), q8f[s], __builtin_bit_cast(i32x16, acc)));
+        else
+          acc = mfma_f16(as_half8(kf[j]), qf[s], acc);
+      }
+      if constexpr (kExp) {   // the 16 exp pairs, spread evenly over the chunks
+        static_for<(16 * j) / NQ, (16 * (j + 1)) / NQ>([&](auto pc) {
+          constexpr int J = decltype(pc)::value;
+          exp_pair<J>(x0, x1, c_x, msub_x, pfr, (J & 1) ? zs1 : zs0);
+        });
+      }
+      if constexpr (kQK == 2 && j > NQ / 2) {   // y0 to float, spread over the late chunks
+        constexpr int kLate = NQ - 1 - NQ / 2, k = j - NQ / 2 - 1;
+        static_for<(16 * k) / kLate, (16 * (k + 1)) / kLate>([&](auto rc) { to_float(y0, decltype(rc)::value); });
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    if constexpr (kQK == 2) {
+      static_for<0, 16>([&](auto rc) { to_float(y1, decltype(rc)::value); });
+    }
+    zs = zs0 + zs1;
   };
+
+  // Phase B: P.V of tile n (when kPV) interleaved with the lane's max of the float scores
+  // y0 / y1 of tile n + 1.
+  auto phase_b = [&](auto pv_tag, int v_off, const half8 (&pfr)[4], const f32x16& y0,
+                     const f32x16& y1) -> float {
+    constexpr bool kPV = decltype(pv_tag)::value;
+    constexpr int NP = kPV ? 4 * (D / 32) : 4;   // chunks
+    constexpr int EP = 32 / NP;                   // score elements per chunk
+    const char* vst = smem + v_off;
+    uint4 vf[NP];
+    auto vload = [&](auto jc) {
+      constexpr int j = decltype(jc)::value, t = j / (D / 32), cc = j % (D / 32);
+      vf[j] = ld_lds_16(vst, fo_128.at(t) + cc * 32 * C::kVRow);
+    };
+    if constexpr (kPV) static_for<0, (kLead < NP ? kLead : NP)>(vload);
+    float mx = -__builtin_huge_valf();
+    static_for<0, NP>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      if constexpr (kPV) {
+        if constexpr (j + kLead < NP) vload(std::integral_constant<int, j + kLead>{});
+        constexpr int t = j / (D / 32), cc = j % (D / 32);
+        oacc[cc] = mfma_f16(as_half8(vf[j]), pfr[t], oacc[cc]);
+      }
+      static_for<0, EP / 2>([&](auto ec) {
+        constexpr int i = j * EP + 2 * decltype(ec)::value;
+        float v0, v1;
+        if constexpr (i < 16) {
+          v0 = y0[i];
+          v1 = y0[i + 1];
+        } else {
+          v0 = y1[i - 16];
+          v1 = y1[i - 15];
+        }
+        mx = max3f(mx, v0, v1);
+      });
+      // An opaque use pins this chunk's share of the max here; otherwise it is sunk past the
+      // MFMAs to where the max is consumed.
+      asm volatile("" ::"v"(mx));
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    return mx;
+  };
+
+  // Max update for tile n + 1 with lane max mx (raw units) and factor c >= 0: running max,
+  // the lazy rescale of the accumulator (only when some row's max grows by more than 2^8), and
+  // the subtrahend and factor of the next exp half.
+  auto max_update = [&](float mx, float c) {
+    const float mt = pair_max(mx) * c;
+    const float m_new = fmaxf(m_run, mt);
+    if (__any(m_new > m_run + kRescaleThreshold)) {
+      const float alpha = (m_new == kNegInf) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+      z_run *= alpha;
+#pragma unroll
+      for (int cc = 0; cc < D / 32; ++cc) oacc[cc] *= alpha;
+      m_run = m_new;
+    }
+    msub = (m_run == kNegInf) ? 0.0f : m_run;
+    c_cur = c;
+  };
+
+  using True = std::integral_constant<bool, true>;
+  using False = std::integral_constant<bool, false>;
+  using QKNone = std::integral_constant<int, 0>;
+  using QKFp16 = std::integral_constant<int, 1>;
+  using QKInt8 = std::integral_constant<int, 2>;
 
   // Tiles whose every key every row of the workgroup may see: keys <= the first row's last key.
   const int wg_first_row_last_key = min(a.Lk - 1, m * BM + off);
   const int n_split = max(0, min(n_end + 1, (wg_first_row_last_key + 1) / kBlockN));
-  using Unmasked = std::integral_constant<bool, false>;
-  using Masked = std::integral_constant<bool, true>;
-  if (!late) {
-    int n = 0;
-    for (; n < n_split; ++n) early_tile(n, Unmasked{});
-    for (; n <= n_end; ++n) early_tile(n, Masked{});
-  } else {
-    float sv_late[32];   // scores of the previous tile, carried across the tile barrier
-    float c_late = 0.0f;
-    // Each tile's softmax uses the same (masked or unmasked) variant as in the early head, so
-    // the two heads compute bit-identical results on identical inputs.
-    auto late_tile = [&](int n, auto prev_masked_tag, auto cur_masked_tag) {
-      constexpr bool kPrevMasked = decltype(prev_masked_tag)::value;
-      constexpr bool kCurMasked = decltype(cur_masked_tag)::value;
-      prefetch(n);
-      if (n >= 1 && sees(n - 1, kPrevMasked)) {
-        half8 pfr[4];
-        softmax_step<D, kPrevMasked>(sv_late, c_late, (n - 1) * kBlockN, my_last_key, lane, m_run,
-                                     z_run, oacc, pfr);
-        pv(n - 1, pfr);
-      }
-      if (sees(n, kCurMasked)) qk(n, sv_late, c_late);
-      finish_tile(n);
-    };
-    int n = 0;
-    for (; n < n_split; ++n) late_tile(n, Unmasked{}, Unmasked{});
-    if (n <= n_end) late_tile(n++, Unmasked{}, Masked{});
-    for (; n <= n_end; ++n) late_tile(n, Masked{}, Masked{});
-    half8 pfr[4];   // the last tile's softmax and P.V
-    if (n_end < n_split) {
-      if (sees(n_end, false)) {
-        softmax_step<D, false>(sv_late, c_late, n_end * kBlockN, my_last_key, lane, m_run, z_run,
-                               oacc, pfr);
-        pv(n_end, pfr);
-      }
-    } else if (sees(n_end, true)) {
-      softmax_step<D, true>(sv_late, c_late, n_end * kBlockN, my_last_key, lane, m_run, z_run,
-                            oacc, pfr);
-      pv(n_end, pfr);
+
+  issue(1, 0);   // K of tiles 0 and 1, V of tile 0
+  wait_all_memory();
+  __syncthreads();
+
+  f32x16 xa0, xa1, xb0, xb1;   // the two score buffers
+  if (n_split > 0 && wave_active) {   // Q K^T and row max of tile 0
+    half8 unused_p[4];
+    float unused_z;
+    const bool int8 = route_of(0);
+    if (int8) phase_a(QKInt8{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
+    else phase_a(QKFp16{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
+    const float mx = phase_b(False{}, 0, unused_p, xa0, xa1);
+    max_update(mx, int8 ? c_int8_q * half_bits_to_float(key_scale[0]) : c_fp16);
+  }
+  // Step n: scores of tile n in x, tile n + 1's go to y.
+  auto step = [&](int n, const f32x16& x0, const f32x16& x1, f32x16& y0, f32x16& y1) {
+    sync(n + 2, n + 1);   // K of tile n + 1 and V of tile n landed; K n + 2, V n + 1 in flight
+    if (!wave_active) return;
+    const bool has_next = n + 1 < n_split;
+    const bool int8 = has_next && route_of(n + 1);
+    const uint16_t ks = key_scale[min(n + 1, n_end)];
+    half8 pfr[4];
+    float zs;
+    if (!has_next) {
+      y0 = f32x16{};
+      y1 = f32x16{};
+      phase_a(QKNone{}, True{}, 0, x0, x1, y0, y1, pfr, zs);
+    } else if (int8) {
+      phase_a(QKInt8{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
+    } else {
+      phase_a(QKFp16{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
+    }
+    z_run += zs;
+    const float mx = phase_b(True{}, v_slot(n), pfr, y0, y1);
+    if (has_next) max_update(mx, int8 ? c_int8_q * half_bits_to_float(ks) : c_fp16);
+  };
+  int n = 0;
+  for (; n + 1 < n_split; n += 2) {
+    step(n, xa0, xa1, xb0, xb1);
+    step(n + 1, xb0, xb1, xa0, xa1);
+  }
+  if (n < n_split) step(n, xa0, xa1, xb0, xb1);
+
+  // Tiles crossing the diagonal or the sequence end, one at a time with the masked softmax;
+  // waves whose rows see no key of a tile skip its math.
+  for (n = n_split; n <= n_end; ++n) {
+    sync(n + 1, n + 1);   // tile n landed; the slots of tile n - 1 take tile n + 1
+    if (wave_active && n * kBlockN <= wave_last_key) {
+      float svm[32], c;
+      qk(n, svm, c);
+      half8 pfr[4];
+      softmax_step<D, true>(svm, c, n * kBlockN, my_last_key, lane, m_run, z_run, oacc, pfr);
+      pv(n, pfr);
     }
   }
 
@@ -602,12 +781,12 @@ __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
   }
 }
 
-template <int D, int BM, int HEADS, int NSTAGE, bool PINGPONG = false>
+template <int D, int BM, int HEADS>
 hipError_t launch_attn_t(const AttnArgs& a, hipStream_t stream) {
   using C = TileCfg<D, BM, HEADS>;
   const long long grid = (long long)a.B * (a.Hq / HEADS) * a.T_m;
   if (grid <= 0 || grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS, NSTAGE, PINGPONG>), dim3((unsigned)grid),
+  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS>), dim3((unsigned)grid),
                      dim3(C::kThreads), 0, stream, a);
   return hipGetLastError();
 }
@@ -622,15 +801,11 @@ hipError_t launch_debug_t(const DebugTileArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_routed_attention(const AttnArgs& a, int d, int block_m, hipStream_t stream) {
-  // d = 128: two query heads of a GQA group per workgroup (one K/V copy serves both) when the
-  // group has an even number of heads, with three LDS stages.  d = 64: one head, four stages.
-  const bool pair = ((a.Hq / a.Hk) % 2) == 0;
-  if (d == 128 && block_m == 128)
-    return pair ? launch_attn_t<128, 128, 2, 3, true>(a, stream) : launch_attn_t<128, 128, 1, 2>(a, stream);
-  if (d == 128 && block_m == 64)
-    return pair ? launch_attn_t<128, 64, 2, 2>(a, stream) : launch_attn_t<128, 64, 1, 2>(a, stream);
-  if (d == 64 && block_m == 128) return launch_attn_t<64, 128, 1, 4>(a, stream);
-  if (d == 64 && block_m == 64) return launch_attn_t<64, 64, 1, 4>(a, stream);
+  // One query head per workgroup; two workgroups share a CU.
+  if (d == 128 && block_m == 128) return launch_attn_t<128, 128, TM_HEADS>(a, stream);
+  if (d == 128 && block_m == 64) return launch_attn_t<128, 64, 1>(a, stream);
+  if (d == 64 && block_m == 128) return launch_attn_t<64, 128, 1>(a, stream);
+  if (d == 64 && block_m == 64) return launch_attn_t<64, 64, 1>(a, stream);
   return hipErrorInvalidValue;
 }
 
