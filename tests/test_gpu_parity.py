@@ -95,6 +95,7 @@ SMALL = [
     ("tiny-L1", dict(B=1, Hq=1, Hk=1, d=128, L=1, block_m=128, group_size=1)),
     ("tiny-L33", dict(B=1, Hq=2, Hk=1, d=64, L=33, block_m=64, group_size=1)),
     ("noncausal", dict(B=1, Hq=2, Hk=1, d=128, L=300, block_m=128, group_size=1, causal=False)),
+    ("gqa3", dict(B=1, Hq=6, Hk=2, d=128, L=260, block_m=128, group_size=2)),
     ("multiword-g1", dict(B=1, Hq=2, Hk=1, d=128, L=4500, block_m=128, group_size=1)),
 ]
 MASKS = [MaskSpec("bernoulli", 0.5), MaskSpec("all_fp16"), MaskSpec("all_int8")]
@@ -167,6 +168,30 @@ def test_workload_parity_sampled(name):
         assert mx <= MAX_ABS and rel <= REL_L2, (name, mask.label, mx, rel)
         del O
         torch.cuda.empty_cache()
+
+
+def test_deviation_from_fp16_matches_oracle():
+    """The routed output's deviation from exact attention (every tile FP16), measured on the GPU,
+    agrees with the oracle's on sampled rows (the figure bench.py reports)."""
+    cfg = WORKLOADS["8k-gqa"]
+    Q, K, V = make_qkv(cfg)
+    dev = (to_dev(Q), to_dev(K), to_dev(V))
+    words, _ = make_route_bits(cfg, cfg.masks[0], 0)
+    zeros = np.zeros_like(words)
+    O_r = prefill(cfg, Q, K, V, words, dev_inputs=dev).float().cpu().numpy()
+    O_f = prefill(cfg, Q, K, V, zeros, route_hint=0, dev_inputs=dev).float().cpu().numpy()
+    rows = sample_rows(cfg)[:2]
+    ops = OracleOperands.from_inputs(Q, K, q_heads=sorted({(b, h) for b, h, _ in rows}),
+                                     k_heads=sorted({(b, h // (cfg.Hq // cfg.Hk)) for b, h, _ in rows}))
+    ref_r = _oracle(cfg, Q, K, V, words, rows, operands=ops)
+    ref_f = _oracle(cfg, Q, K, V, zeros, rows, operands=ops)
+    for (b, h, idx), rr, rf in zip(rows, ref_r, ref_f):
+        gpu_dev = O_r[b, idx, h].astype(np.float64) - O_f[b, idx, h].astype(np.float64)
+        ora_dev = rr - rf
+        log(f"deviation b={b} h={h}: gpu mean_abs {np.abs(gpu_dev).mean():.3e} "
+            f"oracle mean_abs {np.abs(ora_dev).mean():.3e}")
+        assert 1e-6 < np.abs(ora_dev).mean() < 1e-2
+        assert np.abs(gpu_dev - ora_dev).max() <= 2 * MAX_ABS
 
 
 # ------------------------------------------------------------------------ invariants
