@@ -57,6 +57,22 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 constexpr float kRescaleThreshold = 8.0f;   // log2 units: rescale when the max grows > x256
 constexpr float kNegInf = -__builtin_huge_valf();
+// Pipelined tiles do not recompute the row max: P = 2^(score - m) is formed against the
+// running max m as it stands, which only ever holds an actual earlier score maximum, so P
+// cannot underflow relative to the row's mass.  A lane whose 32 FP16 P values sum past this
+// limit (or reach infinity) makes the wave refresh m from the tile's exact max and redo the
+// tile; below it every P is a finite FP16 value well inside range.
+constexpr float kSumLimit = 4096.0f;
+// An INT8 accumulator may start at the bit pattern of 1.5 * 2^23: every exact INT32 product C
+// (|C| <= 128 * 127^2 < 2^21) then leaves it holding the FP32 number 1.5 * 2^23 + C, read as
+// float with no conversion instruction, and the bias is folded into the exp subtrahend
+// k = 1.5 * 2^23 * c + m.  That fold rounds k once, by at most half an ulp of k; a tile takes
+// it only when |k| < kFoldLimit, which keeps the error of the exp argument within 2^-11 (a
+// relative 3.4e-4 on P, below the FP16 rounding P gets anyway).  Other INT8 tiles start at 0
+// and convert the products exactly.
+constexpr int kMagicBits = 0x4B400000;
+constexpr float kMagic = 12582912.0f;
+constexpr float kFoldLimit = 16384.0f;
 
 template <int D, int BM, int HEADS>
 struct TileCfg {
@@ -518,134 +534,128 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
 
   // ---- Software-pipelined path for the tiles every row of the workgroup sees in full.  Each
   // step interleaves, in one wave, matrix-core work of one tile with vector work of another:
-  //   phase A: Q K^T of tile n + 1           | exp half of tile n's softmax (P(n), row sum)
-  //   phase B: O += V^T P^T of tile n (P.V)  | row max of tile n + 1's scores
-  // and the max update (with the rare lazy rescale) closes the step.  Every chunk below is one
-  // MFMA plus its share of the vector work, kept in program order by a scheduling barrier;
-  // LDS fragments are read kLead chunks ahead of the MFMA that consumes them.  A tile's 32
-  // scores per lane live in two accumulator blocks (elements 0-15, 16-31); two such buffers
-  // alternate between "scores of tile n" and "scores of tile n + 1" from step to step.
-  constexpr int kLead = 3;
-  float c_cur = 0.0f;
+  //   phase A: Q K^T of tile n + 1           | exp of tile n's softmax (P(n), row sum)
+  //   phase B: O += V^T P^T of tile n (P.V)
+  // Every chunk below is one MFMA plus its share of the vector work, kept in program order by
+  // a scheduling barrier; LDS fragments are read kLeadA / kLeadB chunks ahead of the MFMA that
+  // consumes them.  A tile's 32 scores per lane live in two accumulator blocks (elements 0-15, 16-31);
+  // two such buffers alternate between "scores of tile n" and "scores of tile n + 1" from
+  // step to step.  Raw scores are FP32 dot products (FP16 route) or 1.5 * 2^23 + C (INT8
+  // route); a tile's log2-domain score is (raw - bias) * c with bias 0 or 1.5 * 2^23, and P
+  // is 2^(raw * c - k) with k = bias * c + msub.
+  constexpr int kLeadA = 2, kLeadB = 3;
+  float c_cur = 0.0f, bias_cur = 0.0f, k_cur = 0.0f;
+  i32x16 magic;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) magic[r] = kMagicBits;
 
-  // Phase A.  QK: 0 = none (exp half only), 1 = FP16 route, 2 = INT8 route for tile n + 1,
-  // whose scores go to y0 / y1 as floats (INT8 route: the exact INT32 products converted).
+  // Phase A.  QK: 0 = none (exp only), 1 = FP16 route, 2 = INT8 route with the folded bias,
+  // 3 = INT8 route with exact conversion, for tile n + 1, whose raw scores go to y0 / y1.
   auto phase_a = [&](auto qk_tag, auto exp_tag, int k_off, const f32x16& x0, const f32x16& x1,
                      f32x16& y0, f32x16& y1, half8 (&pfr)[4], float& zs) {
     constexpr int kQK = decltype(qk_tag)::value;
     constexpr bool kExp = decltype(exp_tag)::value;
-    constexpr int NQ = kQK == 0 ? 4 : (kQK == 2 ? 2 * (D / 32) : 2 * (D / 16));   // chunks
-    // Chunk j feeds accumulator h = j / (NQ/2) with K slice s = j % (NQ/2): y0 is complete
-    // half-way through, and (INT8 route) is converted to float under the MFMAs of y1.
+    constexpr int NQ = kQK == 0 ? 4 : (kQK >= 2 ? 2 * (D / 32) : 2 * (D / 16));   // chunks
+    // Chunk j feeds accumulator h = j % 2 with K slice s = j / 2: consecutive MFMAs write
+    // different accumulators, so none waits for its predecessor's result.
     const char* kst = smem + k_off;
     uint4 kf[NQ];
     auto kload = [&](auto jc) {
-      constexpr int j = decltype(jc)::value, s = j % (NQ / 2), h = j / (NQ / 2);
-      if constexpr (kQK == 2) kf[j] = ld_lds_16(kst, fo_k8.at(s) + h * 32 * D);
+      constexpr int j = decltype(jc)::value, s = j / 2, h = j % 2;
+      if constexpr (kQK >= 2) kf[j] = ld_lds_16(kst, fo_k8.at(s) + h * 32 * D);
       else kf[j] = ld_lds_16(kst, fo_128.at(s & 3) + (s >> 2) * (kBlockN * 128) + h * 32 * 128);
     };
-    if constexpr (kQK != 0) {
-      static_for<0, (kLead < NQ ? kLead : NQ)>(kload);
-      y0 = f32x16{};
-      y1 = f32x16{};
-    }
-    // Every call site computes the same exp half of tile n; an opaque copy of its inputs keeps
+    if constexpr (kQK != 0) static_for<0, (kLeadA < NQ ? kLeadA : NQ)>(kload);
+    // Every call site computes the same exp of tile n; an opaque copy of its inputs keeps
     // each copy inside its own branch, interleaved with that branch's MFMAs, instead of being
     // merged ahead of the branch.
-    float c_x = c_cur, msub_x = msub;
-    asm volatile("" : "+v"(c_x), "+v"(msub_x));
-    auto to_float = [](f32x16& y, int r) {
-      const float raw = y[r];   // (bit-casting the element lvalue itself reads element 0)
-      y[r] = (float)__builtin_bit_cast(int, raw);
-    };
+    float c_x = c_cur, k_x = k_cur;
+    asm volatile("" : "+v"(c_x), "+v"(k_x));
     float zs0 = 0.0f, zs1 = 0.0f;
     static_for<0, NQ>([&](auto jc) {
       constexpr int j = decltype(jc)::value;
       if constexpr (kQK != 0) {
-        if constexpr (j + kLead < NQ) kload(std::integral_constant<int, j + kLead>{});
-        constexpr int s = j % (NQ / 2);
-        f32x16& acc = (j < NQ / 2) ? y0 : y1;
-        if constexpr (kQK == 2)
-          acc = __builtin_bit_cast(
-              f32x16, mfma_i8(as_i32x4(kf[j]), q8f[s], __builtin_bit_cast(i32x16, acc)));
-        else
-          acc = mfma_f16(as_half8(kf[j]), qf[s], acc);
+        if constexpr (j + kLeadA < NQ) kload(std::integral_constant<int, j + kLeadA>{});
+        constexpr int s = j / 2;
+        f32x16& acc = (j % 2 == 0) ? y0 : y1;
+        if constexpr (kQK >= 2) {
+          const i32x16 init = kQK == 2 ? magic : i32x16{};
+          const i32x16 cin = (s == 0) ? init : __builtin_bit_cast(i32x16, acc);
+          acc = __builtin_bit_cast(f32x16, mfma_i8(as_i32x4(kf[j]), q8f[s], cin));
+          if constexpr (kQK == 3 && j >= NQ - 2) {   // exact INT32 -> FP32
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const float raw = acc[r];   // (bit-casting the element lvalue reads element 0)
+              acc[r] = (float)__builtin_bit_cast(int, raw);
+            }
+          }
+        } else {
+          acc = mfma_f16(as_half8(kf[j]), qf[s], s == 0 ? f32x16{} : acc);
+        }
       }
       if constexpr (kExp) {   // the 16 exp pairs, spread evenly over the chunks
         static_for<(16 * j) / NQ, (16 * (j + 1)) / NQ>([&](auto pc) {
           constexpr int J = decltype(pc)::value;
-          exp_pair<J>(x0, x1, c_x, msub_x, pfr, (J & 1) ? zs1 : zs0);
+          exp_pair<J>(x0, x1, c_x, k_x, pfr, (J & 1) ? zs1 : zs0);
         });
-      }
-      if constexpr (kQK == 2 && j > NQ / 2) {   // y0 to float, spread over the late chunks
-        constexpr int kLate = NQ - 1 - NQ / 2, k = j - NQ / 2 - 1;
-        static_for<(16 * k) / kLate, (16 * (k + 1)) / kLate>([&](auto rc) { to_float(y0, decltype(rc)::value); });
       }
       __builtin_amdgcn_sched_barrier(0);
     });
-    if constexpr (kQK == 2) {
-      static_for<0, 16>([&](auto rc) { to_float(y1, decltype(rc)::value); });
-    }
     zs = zs0 + zs1;
   };
 
-  // Phase B: P.V of tile n (when kPV) interleaved with the lane's max of the float scores
-  // y0 / y1 of tile n + 1.
-  auto phase_b = [&](auto pv_tag, int v_off, const half8 (&pfr)[4], const f32x16& y0,
-                     const f32x16& y1) -> float {
-    constexpr bool kPV = decltype(pv_tag)::value;
-    constexpr int NP = kPV ? 4 * (D / 32) : 4;   // chunks
-    constexpr int EP = 32 / NP;                   // score elements per chunk
+  // Phase B: P.V of tile n.
+  auto phase_b = [&](int v_off, const half8 (&pfr)[4]) {
+    constexpr int NP = 4 * (D / 32);   // chunks
     const char* vst = smem + v_off;
     uint4 vf[NP];
     auto vload = [&](auto jc) {
       constexpr int j = decltype(jc)::value, t = j / (D / 32), cc = j % (D / 32);
       vf[j] = ld_lds_16(vst, fo_128.at(t) + cc * 32 * C::kVRow);
     };
-    if constexpr (kPV) static_for<0, (kLead < NP ? kLead : NP)>(vload);
-    float mx = -__builtin_huge_valf();
+    static_for<0, (kLeadB < NP ? kLeadB : NP)>(vload);
     static_for<0, NP>([&](auto jc) {
       constexpr int j = decltype(jc)::value;
-      if constexpr (kPV) {
-        if constexpr (j + kLead < NP) vload(std::integral_constant<int, j + kLead>{});
-        constexpr int t = j / (D / 32), cc = j % (D / 32);
-        oacc[cc] = mfma_f16(as_half8(vf[j]), pfr[t], oacc[cc]);
-      }
-      static_for<0, EP / 2>([&](auto ec) {
-        constexpr int i = j * EP + 2 * decltype(ec)::value;
-        float v0, v1;
-        if constexpr (i < 16) {
-          v0 = y0[i];
-          v1 = y0[i + 1];
-        } else {
-          v0 = y1[i - 16];
-          v1 = y1[i - 15];
-        }
-        mx = max3f(mx, v0, v1);
-      });
-      // An opaque use pins this chunk's share of the max here; otherwise it is sunk past the
-      // MFMAs to where the max is consumed.
-      asm volatile("" ::"v"(mx));
+      if constexpr (j + kLeadB < NP) vload(std::integral_constant<int, j + kLeadB>{});
+      constexpr int t = j / (D / 32), cc = j % (D / 32);
+      oacc[cc] = mfma_f16(as_half8(vf[j]), pfr[t], oacc[cc]);
       __builtin_amdgcn_sched_barrier(0);
     });
-    return mx;
   };
 
-  // Max update for tile n + 1 with lane max mx (raw units) and factor c >= 0: running max,
-  // the lazy rescale of the accumulator (only when some row's max grows by more than 2^8), and
-  // the subtrahend and factor of the next exp half.
-  auto max_update = [&](float mx, float c) {
-    const float mt = pair_max(mx) * c;
-    const float m_new = fmaxf(m_run, mt);
-    if (__any(m_new > m_run + kRescaleThreshold)) {
-      const float alpha = (m_new == kNegInf) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
-      z_run *= alpha;
+  // Lane max of a tile's 32 raw scores.
+  auto lane_max = [](const f32x16& y0, const f32x16& y1) {
+    float mx = max3f(y0[0], y0[1], y0[2]);
 #pragma unroll
-      for (int cc = 0; cc < D / 32; ++cc) oacc[cc] *= alpha;
-      m_run = m_new;
-    }
-    msub = (m_run == kNegInf) ? 0.0f : m_run;
-    c_cur = c;
+    for (int i = 3; i < 15; i += 2) mx = max3f(mx, y0[i], y0[i + 1]);
+    mx = max3f(mx, y0[15], y1[0]);
+#pragma unroll
+    for (int i = 1; i < 15; i += 2) mx = max3f(mx, y1[i], y1[i + 1]);
+    return fmaxf(mx, y1[15]);
+  };
+
+  // Raise the running max to the tile max mt (log2 units) where it is larger, rescaling the
+  // accumulator and the normalizer by 2^(m_old - m_new), and re-derive the exp subtrahend.
+  auto raise_max = [&](float mt) {
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = (m_run == kNegInf) ? 0.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+    z_run *= alpha;
+#pragma unroll
+    for (int cc = 0; cc < D / 32; ++cc) oacc[cc] *= alpha;
+    m_run = m_new;
+    msub = m_run;
+    k_cur = fmaf(bias_cur, c_cur, msub);
+  };
+  // Factor and bias of key tile t's raw scores.
+  auto set_tile = [&](bool int8, bool fold, uint16_t ks) {
+    c_cur = int8 ? c_int8_q * half_bits_to_float(ks) : c_fp16;
+    bias_cur = fold ? kMagic : 0.0f;
+    k_cur = fmaf(bias_cur, c_cur, msub);
+  };
+  // Whether an INT8 tile with key scale ks takes the folded bias (same decision in every lane).
+  auto fold_ok = [&](uint16_t ks) {
+    const float c = c_int8_q * half_bits_to_float(ks);
+    return !__any(!(fmaf(kMagic, c, fabsf(msub)) < kFoldLimit));
   };
 
   using True = std::integral_constant<bool, true>;
@@ -653,6 +663,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   using QKNone = std::integral_constant<int, 0>;
   using QKFp16 = std::integral_constant<int, 1>;
   using QKInt8 = std::integral_constant<int, 2>;
+  using QKInt8Exact = std::integral_constant<int, 3>;
 
   // Tiles whose every key every row of the workgroup may see: keys <= the first row's last key.
   const int wg_first_row_last_key = min(a.Lk - 1, m * BM + off);
@@ -663,14 +674,16 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   __syncthreads();
 
   f32x16 xa0, xa1, xb0, xb1;   // the two score buffers
-  if (n_split > 0 && wave_active) {   // Q K^T and row max of tile 0
+  if (n_split > 0 && wave_active) {   // Q K^T of tile 0 and the running max it starts
     half8 unused_p[4];
     float unused_z;
     const bool int8 = route_of(0);
-    if (int8) phase_a(QKInt8{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
+    const bool fold = int8 && fold_ok(key_scale[0]);
+    if (fold) phase_a(QKInt8{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
+    else if (int8) phase_a(QKInt8Exact{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
     else phase_a(QKFp16{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
-    const float mx = phase_b(False{}, 0, unused_p, xa0, xa1);
-    max_update(mx, int8 ? c_int8_q * half_bits_to_float(key_scale[0]) : c_fp16);
+    set_tile(int8, fold, key_scale[0]);
+    raise_max((pair_max(lane_max(xa0, xa1)) - bias_cur) * c_cur);
   }
   // Step n: scores of tile n in x, tile n + 1's go to y.
   auto step = [&](int n, const f32x16& x0, const f32x16& x1, f32x16& y0, f32x16& y1) {
@@ -679,20 +692,30 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     const bool has_next = n + 1 < n_split;
     const bool int8 = has_next && route_of(n + 1);
     const uint16_t ks = key_scale[min(n + 1, n_end)];
+    const bool fold = int8 && fold_ok(ks);
     half8 pfr[4];
     float zs;
     if (!has_next) {
       y0 = f32x16{};
       y1 = f32x16{};
       phase_a(QKNone{}, True{}, 0, x0, x1, y0, y1, pfr, zs);
-    } else if (int8) {
+    } else if (fold) {
       phase_a(QKInt8{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
+    } else if (int8) {
+      phase_a(QKInt8Exact{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
     } else {
       phase_a(QKFp16{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
     }
+    if (__builtin_expect(__any(!(zs <= kSumLimit)), 0)) {
+      // Some P of tile n left the comfortable FP16 range: refresh the running max from the
+      // tile's exact max and redo its exp.
+      raise_max((pair_max(lane_max(x0, x1)) - bias_cur) * c_cur);
+      f32x16 u0, u1;
+      phase_a(QKNone{}, True{}, 0, x0, x1, u0, u1, pfr, zs);
+    }
     z_run += zs;
-    const float mx = phase_b(True{}, v_slot(n), pfr, y0, y1);
-    if (has_next) max_update(mx, int8 ? c_int8_q * half_bits_to_float(ks) : c_fp16);
+    phase_b(v_slot(n), pfr);
+    if (has_next) set_tile(int8, fold, ks);
   };
   int n = 0;
   for (; n + 1 < n_split; n += 2) {

@@ -202,27 +202,80 @@ def _inv_cfg(**kw):
     return small_workload("inv", index=500, **base)
 
 
-def test_integer_inputs_int8_equals_fp16_bitwise():
+def _integer_inputs(L=512):
     rng = np.random.default_rng(9)
-    cfg = _inv_cfg(L=512)
-    Q = rng.integers(-127, 128, size=(1, 512, 4, 128)).astype(np.float16)
-    K = rng.integers(-127, 128, size=(1, 512, 2, 128)).astype(np.float16)
-    Q[:, ::128, :, 0] = 127.0
-    K[:, ::64, :, 0] = -127.0
-    V = rng.standard_normal((1, 512, 2, 128)).astype(np.float16)
-    cfg = cfg.with_(L=512)
-    w16, _ = make_route_bits(cfg, MaskSpec("all_fp16"))
-    w8, _ = make_route_bits(cfg, MaskSpec("all_int8"))
-    # tiny scale keeps the integer scores in a softmax-friendly range
-    cfg = cfg.with_(d=128)
+    Q = rng.integers(-127, 128, size=(1, L, 4, 128)).astype(np.float16)
+    K = rng.integers(-127, 128, size=(1, L, 2, 128)).astype(np.float16)
+    Q[:, ::128, :, 0] = 127.0     # every 128-row query block and 64-row key block has
+    K[:, ::64, :, 0] = -127.0     # absmax 127, so its scale is 1 and its codes are the inputs
+    V = rng.standard_normal((1, L, 2, 128)).astype(np.float16)
+    return Q, K, V
+
+
+def _both_routes(cfg, Q, K, V, scale):
     import paper_2608_17336_amd as tm
     import torch
+    w16, _ = make_route_bits(cfg, MaskSpec("all_fp16"))
+    w8, _ = make_route_bits(cfg, MaskSpec("all_int8"))
     outs = []
     for w in (w16, w8):
-        O = tm.tilemix_prefill(to_dev(Q), to_dev(K), to_dev(V), to_dev(w), 1, (128, 64), True, 1.0 / 4000.0)
+        O = tm.tilemix_prefill(to_dev(Q), to_dev(K), to_dev(V), to_dev(w), 1, (128, 64), True, scale)
         torch.cuda.synchronize()
-        outs.append(O.cpu().numpy())
-    np.testing.assert_array_equal(outs[0].view(np.uint16), outs[1].view(np.uint16))
+        outs.append(O)
+    return outs, w16
+
+
+def test_integer_inputs_int8_equals_fp16_bitwise():
+    # With scale 1 blocks the INT8 route computes exactly the FP16 route's products.  At this
+    # softmax scale (1.5 * 2^23 * scale * log2(e) >= 2^14) the kernel converts the INT32
+    # products exactly instead of folding the accumulator bias, so the two routes must agree
+    # bit for bit (integer scores reach thousands of log2 units: this also drives the running-
+    # max refresh many times per row).
+    L = 512
+    Q, K, V = _integer_inputs(L)
+    cfg = _inv_cfg(L=L)
+    scale = 1.0 / 512.0
+    outs, _ = _both_routes(cfg, Q, K, V, scale)
+    a, b = (o.cpu().numpy() for o in outs)
+    np.testing.assert_array_equal(a.view(np.uint16), b.view(np.uint16))
+
+
+def test_integer_inputs_folded_bias_within_bound():
+    # At a smaller scale the INT8 tiles fold the accumulator bias into the exp subtrahend, which
+    # rounds the exp argument by at most 2^-11 (log2 units): the routes then agree within the
+    # parity bar, and both match the oracle (where the routes coincide exactly).
+    L = 512
+    Q, K, V = _integer_inputs(L)
+    cfg = _inv_cfg(L=L)
+    scale = 1.0 / 4000.0
+    outs, w16 = _both_routes(cfg, Q, K, V, scale)
+    rows = [(0, h, np.arange(L)) for h in range(4)]
+    ref = routed_attention_rows(Q, K, V, w16, block_m=128, block_n=64, group_size=1, causal=True,
+                                scale=scale, rows=rows)
+    for O in outs:
+        mx, rel = compare_rows(O, rows, ref)
+        log(f"  max_abs={mx:.3e} rel_l2={rel:.3e}")
+        assert mx <= MAX_ABS and rel <= REL_L2, (mx, rel)
+    a, b = (o.float().cpu().numpy() for o in outs)
+    assert float(np.max(np.abs(a - b))) <= MAX_ABS
+
+
+def test_running_max_refresh():
+    # Keys whose norm grows along the sequence make every later tile's scores exceed the
+    # running max taken from the first tile by far more than FP16 P can hold, so the kernel
+    # must refresh the max (and rescale its accumulators) many times per row.
+    cfg = _inv_cfg(L=1024, group_size=1)
+    Q, K, V = make_qkv(cfg)
+    grow = (1.0 + np.arange(cfg.L, dtype=np.float32) / 48.0)[None, :, None, None]
+    K = (K.astype(np.float32) * grow).astype(np.float16)
+    for mi, mask in enumerate(MASKS):
+        words, _ = make_route_bits(cfg, mask, mi)
+        O = prefill(cfg, Q, K, V, words)
+        rows = [(0, h, np.arange(cfg.L)) for h in range(cfg.Hq)]
+        ref = _oracle(cfg, Q, K, V, words, rows)
+        mx, rel = compare_rows(O, rows, ref)
+        log(f"  refresh mask={mask.label} max_abs={mx:.3e} rel_l2={rel:.3e}")
+        assert mx <= MAX_ABS and rel <= REL_L2, (mask.label, mx, rel)
 
 
 def test_first_row_equals_v0_and_route_hint():
