@@ -116,6 +116,10 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="32k-gqa")
     ap.add_argument("--mask", type=int, default=0, help="index into the workload's masks")
+    ap.add_argument("--template", default="",
+                    help="route with a routing template of the library instead of the workload's "
+                         "mask: KIND[:RHO] (KIND one of one, zero, band, global, rowrand, aligned, "
+                         "bigbird, sptrans; RHO the INT8 coverage to fit, default 0.75)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="cap on oracle rows (0 = default sample)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -142,14 +146,32 @@ def main(argv=None):
 
     t0 = time.perf_counter()
     Q, K, V = make_qkv(cfg)
-    words, R = make_route_bits(cfg, mask, args.mask)
-    stats = route_stats(cfg, R)
-    log(f"[bench] inputs for {cfg.name} mask={mask.label} generated in {time.perf_counter() - t0:.1f}s; "
+    mask_label = mask.label
+    mask_kind = mask.kind
+    if args.template:
+        kind, _, rho = args.template.partition(":")
+        rho = float(rho) if rho else 0.75
+        tp = tm.Params(cfg.B, cfg.Hq, cfg.Hk, cfg.L, cfg.L, cfg.d, cfg.block_m, cfg.block_n,
+                       cfg.group_size, cfg.causal, cfg.scale)
+        # SpTrans: stride of sqrt(L) tokens rounded to whole key groups
+        span = cfg.group_size * cfg.block_n
+        stride = max(span, int(round(math.sqrt(cfg.L) / span)) * span)
+        tmpl = tm.tilemix_fit_template(tp, tm.Template(kind, sp_stride=stride, seed=cfg.seed), rho)
+        words = tm.tilemix_route_template(tp, tmpl)
+        rho_g, rho_p = tm.tilemix_route_coverage(tp, words)
+        stats = {"rho_hat": rho_g, "rho_pairs": rho_p}
+        mask_label = f"template:{kind}@{rho:g}"
+        mask_kind = "all_fp16" if kind == "zero" else kind
+        log(f"[bench] template {tmpl}")
+    else:
+        words, R = make_route_bits(cfg, mask, args.mask)
+        stats = route_stats(cfg, R)
+    log(f"[bench] inputs for {cfg.name} mask={mask_label} generated in {time.perf_counter() - t0:.1f}s; "
         f"rho_hat={stats['rho_hat']:.4f} rho_pairs={stats['rho_pairs']:.4f}")
     to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     q, k, v = to(Q), to(K), to(V)
     w = to(words.view(np.int64))
-    hint = 0 if mask.kind == "all_fp16" else -1
+    hint = 0 if mask_kind == "all_fp16" else -1
     kw = dict(group_size=cfg.group_size, tile=(cfg.block_m, cfg.block_n), causal=cfg.causal,
               scale=cfg.scale, route_hint=hint)
     p = tm.Params(cfg.B, cfg.Hq, cfg.Hk, cfg.L, cfg.L, cfg.d, cfg.block_m, cfg.block_n,
@@ -237,7 +259,7 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": cfg.name, "B": cfg.B, "Hq": cfg.Hq, "Hk": cfg.Hk, "d": cfg.d,
                    "L": cfg.L, "causal": cfg.causal, "tile": f"{cfg.block_m}x{cfg.block_n}",
-                   "group_size": cfg.group_size, "mask": mask.label,
+                   "group_size": cfg.group_size, "mask": mask_label,
                    "rho_hat": round(stats["rho_hat"], 4), "rho_pairs": round(stats["rho_pairs"], 4)},
         "pct_of_weighted_roofline": round(100.0 * fm["t_star_s"] / (ms_per_step * 1e-3), 2),
         "attention_ms": round(attn_avg, 4),

@@ -154,6 +154,75 @@ tilemix_status tilemix_debug_qk_int32(const tilemix_params* params, const int8_t
                                       const int8_t* K8, const int32_t* tiles, int32_t count,
                                       int32_t* out, void* stream);
 
+/* ------------------------------------------------------------------ routing templates
+ * Host-side routing policies of Appendix B ("Policy Construction and Sharing", "Coverage
+ * Accounting" and the layouts One, Zero, Band, Global, Row-Random, Aligned Sparse, BigBird,
+ * SpTrans).  A template is a data-free 2-D map R[m, g_j] over query-tile rows m and key-tile
+ * groups g_j (1 = INT8, 0 = FP16), broadcast over KV heads (and sequences) and packed into the
+ * routing words tilemix_prefill reads.  Row m's legal groups G_m are the groups holding at
+ * least one legal (query, key) pair of the row (a prefix 0 .. gmax(m) of the groups); each
+ * layout picks its FP16 set F_m inside G_m, every other legal group is INT8 and every illegal
+ * group's bit is 0.  These functions run on the host only and touch no device memory.
+ */
+typedef enum tilemix_template_kind {
+  TILEMIX_TEMPLATE_ONE = 0,      /* F_m empty: every legal group INT8 */
+  TILEMIX_TEMPLATE_ZERO = 1,     /* F_m = G_m: every legal group FP16 */
+  TILEMIX_TEMPLATE_BAND = 2,     /* F_m = {g_j : |g_j - gamma(m)| <= band_w},
+                                    gamma(m) = floor(m BLOCK_M / (g BLOCK_N)) */
+  TILEMIX_TEMPLATE_GLOBAL = 3,   /* F_m = {g_j < global_groups} (the first key groups) */
+  TILEMIX_TEMPLATE_ROWRAND = 4,  /* F_m = k_m groups of G_m drawn uniformly without replacement,
+                                    k_m = floor(rand_fp16 |G_m| + 1/2); draw order: ascending
+                                    SplitMix64 output of seed ^ (m << 32 | g_j), ties by g_j */
+  TILEMIX_TEMPLATE_ALIGNED = 5,  /* F_m = the last a(m) = min(|G_m|, ceil(align_alpha +
+                                    align_beta m)) groups of G_m (right-aligned) */
+  TILEMIX_TEMPLATE_BIGBIRD = 6,  /* union of Band(band_w; none if -1), Global(global_groups)
+                                    and Row-Random(rand_fp16, seed) */
+  TILEMIX_TEMPLATE_SPTRANS = 7   /* F_m = groups meeting, for some query i of row m, the keys
+                                    [u s, i'] and [max(r s, (r+1) s - c), (r+1) s - 1] for r < u,
+                                    u = floor(i' / s), i' = i + L_k - L_q, s = sp_stride,
+                                    c = sp_tail (tokens) */
+} tilemix_template_kind;
+
+typedef struct tilemix_template {
+  int32_t kind;            /* tilemix_template_kind */
+  int32_t band_w;          /* Band (>= 0), BigBird (>= -1): half-width in groups */
+  int32_t global_groups;   /* Global, BigBird: number of leading FP16 groups (>= 0) */
+  float rand_fp16;         /* Row-Random, BigBird: FP16 share of each row, 1 - rho (in [0, 1]) */
+  float align_alpha;       /* Aligned Sparse: initial width */
+  float align_beta;        /* Aligned Sparse: growth per query-tile row */
+  int32_t sp_stride;       /* SpTrans: stride s in tokens (>= 1) */
+  int32_t sp_tail;         /* SpTrans: tail c in tokens (>= 0) */
+  uint64_t seed;           /* Row-Random, BigBird */
+} tilemix_template;
+
+/* The paper's automatic group size: b_64 = ceil(L_k / 64), BLOCK_N^mask = BLOCK_N *
+ * ceil(max(b_64, BLOCK_N) / BLOCK_N), g = BLOCK_N^mask / BLOCK_N (Appendix B).  0 if an
+ * argument is < 1. */
+int32_t tilemix_auto_group_size(int32_t len_k, int32_t block_n);
+
+/* Instantiate a template for `params` (lengths, tile, g, causal, route_per_batch) into HOST
+ * memory `words`, uint64 [B_r, H_k, T_m, W] (B_r as for tilemix_prefill), every plane the
+ * same map; illegal groups and padding bits are 0.  Errors: NULL pointers, invalid params or
+ * template fields. */
+tilemix_status tilemix_route_template(const tilemix_params* params, const tilemix_template* tmpl,
+                                      uint64_t* words);
+
+/* Realized coverage of HOST routing words [B_r, H_k, T_m, W] (Appendix B, "Coverage
+ * Accounting"): rho_groups = INT8 share of the legal (h_k, m, g_j) groups; rho_pairs = INT8
+ * share of the legal (query, key) pairs (over KV heads; each serves H_q / H_k query heads
+ * alike). */
+tilemix_status tilemix_route_coverage(const tilemix_params* params, const uint64_t* words,
+                                      double* rho_groups, double* rho_pairs);
+
+/* Choose the template's size parameter so that its realized group coverage is closest to
+ * rho_int8 (Appendix B: parameters are selected at tile-group granularity to match the
+ * requested coverage).  Band: band_w; Global: global_groups; Row-Random: rand_fp16 = 1 -
+ * rho_int8; Aligned Sparse: align_beta with align_alpha = 1; BigBird: rand_fp16 with band_w = 0
+ * and global_groups = 1; SpTrans: sp_tail for the given sp_stride (>= 1).  One and Zero are
+ * left as they are. */
+tilemix_status tilemix_fit_template(const tilemix_params* params, tilemix_template* tmpl,
+                                    double rho_int8);
+
 /* Static description of a status code. */
 const char* tilemix_status_string(tilemix_status status);
 

@@ -26,6 +26,12 @@ __all__ = [
     "tilemix_attend",
     "tilemix_quantize",
     "tilemix_debug_qk_int32",
+    "Template",
+    "TEMPLATE_KINDS",
+    "tilemix_auto_group_size",
+    "tilemix_route_template",
+    "tilemix_route_coverage",
+    "tilemix_fit_template",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -37,6 +43,10 @@ EXPORTED_SYMBOLS = (
     "tilemix_attend",
     "tilemix_quantize",
     "tilemix_debug_qk_int32",
+    "tilemix_auto_group_size",
+    "tilemix_route_template",
+    "tilemix_route_coverage",
+    "tilemix_fit_template",
     "tilemix_status_string",
     "tilemix_last_error",
 )
@@ -105,6 +115,47 @@ class Params:
         return -(-self.len_k // self.block_n)
 
 
+TEMPLATE_KINDS = {"one": 0, "zero": 1, "band": 2, "global": 3, "rowrand": 4, "aligned": 5,
+                  "bigbird": 6, "sptrans": 7}
+
+
+class _CTemplate(ctypes.Structure):
+    _fields_ = [
+        ("kind", ctypes.c_int32),
+        ("band_w", ctypes.c_int32),
+        ("global_groups", ctypes.c_int32),
+        ("rand_fp16", ctypes.c_float),
+        ("align_alpha", ctypes.c_float),
+        ("align_beta", ctypes.c_float),
+        ("sp_stride", ctypes.c_int32),
+        ("sp_tail", ctypes.c_int32),
+        ("seed", ctypes.c_uint64),
+    ]
+
+
+@dataclass(frozen=True)
+class Template:
+    """Mirror of ``tilemix_template`` (routing layouts of Appendix B)."""
+    kind: str
+    band_w: int = 0
+    global_groups: int = 0
+    rand_fp16: float = 0.0
+    align_alpha: float = 0.0
+    align_beta: float = 0.0
+    sp_stride: int = 0
+    sp_tail: int = 0
+    seed: int = 0
+
+    def c(self) -> _CTemplate:
+        return _CTemplate(TEMPLATE_KINDS[self.kind], self.band_w, self.global_groups, self.rand_fp16,
+                          self.align_alpha, self.align_beta, self.sp_stride, self.sp_tail, self.seed)
+
+    @staticmethod
+    def from_c(kind: str, t: _CTemplate) -> "Template":
+        return Template(kind, t.band_w, t.global_groups, t.rand_fp16, t.align_alpha, t.align_beta,
+                        t.sp_stride, t.sp_tail, t.seed)
+
+
 _LIB = None
 
 
@@ -133,6 +184,16 @@ def load_library() -> ctypes.CDLL:
     lib.tilemix_quantize.restype = ctypes.c_int
     lib.tilemix_debug_qk_int32.argtypes = [P, vp, vp, vp, ctypes.c_int32, vp, vp]
     lib.tilemix_debug_qk_int32.restype = ctypes.c_int
+    TP = ctypes.POINTER(_CTemplate)
+    lib.tilemix_auto_group_size.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    lib.tilemix_auto_group_size.restype = ctypes.c_int32
+    lib.tilemix_route_template.argtypes = [P, TP, vp]
+    lib.tilemix_route_template.restype = ctypes.c_int
+    lib.tilemix_route_coverage.argtypes = [P, vp, ctypes.POINTER(ctypes.c_double),
+                                           ctypes.POINTER(ctypes.c_double)]
+    lib.tilemix_route_coverage.restype = ctypes.c_int
+    lib.tilemix_fit_template.argtypes = [P, TP, ctypes.c_double]
+    lib.tilemix_fit_template.restype = ctypes.c_int
     lib.tilemix_status_string.argtypes = [ctypes.c_int]
     lib.tilemix_status_string.restype = ctypes.c_char_p
     lib.tilemix_last_error.argtypes = []
@@ -298,3 +359,46 @@ def tilemix_debug_qk_int32(Q8, K8, tiles, *, heads_q: int, heads_kv: int, tile=(
     _check(load_library().tilemix_debug_qk_int32(ctypes.byref(cp), _ptr(Q8), _ptr(K8), _ptr(tiles),
                                                  ctypes.c_int32(count), _ptr(out), _stream(stream)))
     return out
+
+
+# ----------------------------------------------------------------- routing templates (host)
+
+def tilemix_auto_group_size(len_k: int, block_n: int = 64) -> int:
+    """The paper's automatic routing-group size g for L_k keys (0 if an argument is < 1)."""
+    return int(load_library().tilemix_auto_group_size(len_k, block_n))
+
+
+def _host_words_shape(p: Params):
+    return (p.batch if p.route_per_batch else 1, p.heads_kv, p.T_m, tilemix_route_words_per_row(p))
+
+
+def tilemix_route_template(params: Params, template: Template):
+    """Routing words (host NumPy uint64 [B_r, H_k, T_m, W]) of ``template`` for ``params``."""
+    import numpy as np
+    shape = _host_words_shape(params)
+    words = np.zeros(shape, dtype=np.uint64)
+    cp, ct = params.c(), template.c()
+    _check(load_library().tilemix_route_template(ctypes.byref(cp), ctypes.byref(ct),
+                                                 words.ctypes.data_as(ctypes.c_void_p)))
+    return words
+
+
+def tilemix_route_coverage(params: Params, words):
+    """(rho_groups, rho_pairs): realized INT8 coverage of host routing words."""
+    import numpy as np
+    w = np.ascontiguousarray(words, dtype=np.uint64)
+    if w.shape != _host_words_shape(params):
+        raise ValueError(f"words must have shape {_host_words_shape(params)}, got {w.shape}")
+    rg, rp = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    cp = params.c()
+    _check(load_library().tilemix_route_coverage(ctypes.byref(cp), w.ctypes.data_as(ctypes.c_void_p),
+                                                 ctypes.byref(rg), ctypes.byref(rp)))
+    return rg.value, rp.value
+
+
+def tilemix_fit_template(params: Params, template: Template, rho_int8: float) -> Template:
+    """The template with its size parameter chosen to match INT8 coverage ``rho_int8``."""
+    cp, ct = params.c(), template.c()
+    _check(load_library().tilemix_fit_template(ctypes.byref(cp), ctypes.byref(ct),
+                                               ctypes.c_double(rho_int8)))
+    return Template.from_c(template.kind, ct)

@@ -9,14 +9,17 @@
 //   2. computes the transposed score tile S^T (keys x queries) on the matrix cores:
 //        FP16 route: v_mfma_f32_32x32x16_f16, K from LDS x Q from registers;
 //        INT8 route: v_mfma_i32_32x32x32_i8 on the quantize-once codes, exact INT32,
-//                    then one FP32 factor scale*log2(e)*dQ*dK (Appendix C rescale);
+//                    then one FP32 factor scale*log2(e)*dQ*dK (Appendix C rescale),
+//                    applied in the exp argument;
 //      with keys on the matrix rows, every lane holds all scores of one query row for
 //      16 keys of each 32-key block, so row max / row sum are in-lane plus one exchange
 //      between the two half-waves;
 //   3. updates the shared online-softmax state of Section 3.1 in FP32 (running max in
-//      the log2 domain, normalizer, output accumulator).  The accumulator is rescaled
-//      only when a row's max grows by more than 2^8, which leaves the result unchanged
-//      and keeps P <= 256 in FP16;
+//      the log2 domain, normalizer, output accumulator).  Tiles that every row sees in full
+//      form P against the running max as it stands and refresh it (rescaling the
+//      accumulator) only when a lane's FP16 P sum passes a limit; tiles that cross the
+//      diagonal use their exact max and rescale when it grows by more than 2^8.  Either
+//      way the result is the same softmax;
 //   4. packs P to FP16 in registers, in exactly the operand layout the P.V step needs,
 //      and accumulates O^T += V^T P^T (v_mfma_f32_32x32x16_f16, FP32 accumulate).
 // Legality (causal, sequence end) is applied only on tiles that cross it; tiles past

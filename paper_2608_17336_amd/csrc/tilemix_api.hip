@@ -10,11 +10,15 @@
 #include "tilemix_device.h"
 #include "tilemix_internal.h"
 
+namespace tilemix {
+namespace api {
+
 namespace {
-
 thread_local char g_last_error[512] = "";
+}  // namespace
 
-tilemix_status fail(tilemix_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+const char* last_error() { return g_last_error; }
+
 tilemix_status fail(tilemix_status st, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
@@ -28,16 +32,9 @@ tilemix_status ok() {
   return TILEMIX_OK;
 }
 
-size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
-
-// Derived sizes of one problem.
-struct Plan {
-  long long T_m, T_n, T_mask, W;
-  long long nQB, nKB;
-  size_t q8_bytes, k8_bytes, dq_bytes, dk_bytes, vt_bytes;
-  size_t q8_off, k8_off, dq_off, dk_off, vt_off, total;
-};
+namespace {
+long long cdiv_ll(long long a, long long b) { return (a + b - 1) / b; }
+}  // namespace
 
 tilemix_status validate(const tilemix_params* p) {
   if (!p) return fail(TILEMIX_ERR_NULL, "params is NULL");
@@ -64,15 +61,35 @@ tilemix_status validate(const tilemix_params* p) {
   const long long rows_k = (long long)p->batch * p->len_k * p->heads_kv;
   if (rows_q * p->head_dim > (1LL << 40) || rows_k * p->head_dim > (1LL << 40))
     return fail(TILEMIX_ERR_SHAPE, "tensor too large");
-  if (cdiv(p->len_k, p->block_n) > tilemix::kMaxKeyTiles)
+  if (cdiv_ll(p->len_k, p->block_n) > tilemix::kMaxKeyTiles)
     return fail(TILEMIX_ERR_UNSUPPORTED, "len_k %d exceeds the supported %d keys", p->len_k,
                 tilemix::kMaxKeyTiles * tilemix::kBlockN);
-  const long long grid = (long long)p->batch * p->heads_q * cdiv(p->len_q, p->block_m);
+  const long long grid = (long long)p->batch * p->heads_q * cdiv_ll(p->len_q, p->block_m);
   if (grid > 0x7fffffffLL) return fail(TILEMIX_ERR_SHAPE, "too many query tiles");
   if ((long long)p->heads_kv * p->batch > 65535 || p->heads_q > 65535)
     return fail(TILEMIX_ERR_SHAPE, "too many heads");
   return TILEMIX_OK;
 }
+
+}  // namespace api
+}  // namespace tilemix
+
+namespace {
+
+using tilemix::api::fail;
+using tilemix::api::ok;
+using tilemix::api::validate;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
+
+// Derived sizes of one problem.
+struct Plan {
+  long long T_m, T_n, T_mask, W;
+  long long nQB, nKB;
+  size_t q8_bytes, k8_bytes, dq_bytes, dk_bytes, vt_bytes;
+  size_t q8_off, k8_off, dq_off, dk_off, vt_off, total;
+};
 
 Plan make_plan(const tilemix_params* p) {
   Plan pl{};
@@ -291,6 +308,6 @@ const char* tilemix_status_string(tilemix_status status) {
   return "unknown status";
 }
 
-const char* tilemix_last_error(void) { return g_last_error; }
+const char* tilemix_last_error(void) { return tilemix::api::last_error(); }
 
 }  // extern "C"

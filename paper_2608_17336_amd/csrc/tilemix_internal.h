@@ -5,7 +5,19 @@
 #include <stdint.h>
 #include <stddef.h>
 
+#include "tilemix.h"
+
 namespace tilemix {
+
+namespace api {
+// Record a printf-style message as the calling thread's last error and return `st`.
+tilemix_status fail(tilemix_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+// Clear the calling thread's last error and return TILEMIX_OK.
+tilemix_status ok();
+const char* last_error();
+// Check a parameter block (sizes, supported shapes, flags); TILEMIX_OK or an error status.
+tilemix_status validate(const tilemix_params* p);
+}  // namespace api
 
 // Arguments of the fused routed attention kernel (plain values; passed by value).
 struct AttnArgs {

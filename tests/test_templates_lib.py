@@ -1,0 +1,119 @@
+"""The library's host-side routing templates (C ABI) against the template oracle: packed
+words bit for bit, realized coverage, the automatic group size and parameter fitting.  These
+functions run on the host, so the checks run on the CPU."""
+
+import os
+
+import numpy as np
+import pytest
+
+import paper_2608_17336_amd as tm
+from oracle.templates import Geometry, auto_group_size, coverage, pack_words, template_map
+
+pytestmark = pytest.mark.skipif(not os.path.exists(tm.library_path()),
+                                reason="libtilemix.so not built (run __graft_entry__.build())")
+
+# (len_q, len_k, block_m, group_size, causal, heads_kv, batch, route_per_batch)
+GEOMS = [
+    (1000, 1000, 128, 2, True, 2, 1, False),
+    (333, 333, 64, 1, True, 1, 2, True),
+    (300, 500, 128, 3, True, 2, 1, False),      # L_q < L_k: bottom-right causal
+    (500, 300, 64, 1, True, 1, 1, False),       # L_q > L_k: leading rows see no key
+    (260, 260, 128, 1, False, 1, 1, False),     # full attention
+    (4300, 4300, 128, 1, True, 1, 1, False),    # 68 groups: two words per row
+]
+
+TEMPLATES = [
+    ("one", {}), ("zero", {}),
+    ("band", dict(band_w=0)), ("band", dict(band_w=2)),
+    ("global", dict(global_groups=1)), ("global", dict(global_groups=3)),
+    ("rowrand", dict(rand_fp16=0.25, seed=7)), ("rowrand", dict(rand_fp16=0.6, seed=123456789)),
+    ("aligned", dict(align_alpha=1.0, align_beta=0.5)), ("aligned", dict(align_alpha=2.5, align_beta=0.0)),
+    ("bigbird", dict(band_w=0, global_groups=1, rand_fp16=0.2, seed=3)),
+    ("bigbird", dict(band_w=-1, global_groups=2, rand_fp16=0.1, seed=9)),
+    ("sptrans", dict(sp_stride=256, sp_tail=64)), ("sptrans", dict(sp_stride=200, sp_tail=0)),
+    ("sptrans", dict(sp_stride=64, sp_tail=64)),
+]
+
+
+def _params(g):
+    Lq, Lk, bm, gs, causal, hk, b, rpb = g
+    return tm.Params(b, 2 * hk, hk, Lq, Lk, 128, bm, 64, gs, causal, 0.0884, rpb)
+
+
+def _geo(g):
+    Lq, Lk, bm, gs, causal, *_ = g
+    return Geometry(Lq, Lk, bm, 64, gs, causal)
+
+
+@pytest.mark.parametrize("g", GEOMS, ids=[f"{x[0]}x{x[1]}-bm{x[2]}-g{x[3]}-c{int(x[4])}" for x in GEOMS])
+def test_templates_match_oracle(g):
+    p, geo = _params(g), _geo(g)
+    planes = p.batch if p.route_per_batch else 1
+    for kind, kw in TEMPLATES:
+        if kind == "sptrans" and g[0] > 2000 and kw["sp_stride"] < 128:
+            continue
+        words = tm.tilemix_route_template(p, tm.Template(kind, **kw))
+        R = template_map(geo, kind, **kw)
+        want = pack_words(R, p.heads_kv, planes)
+        np.testing.assert_array_equal(words, want, err_msg=f"{kind} {kw}")
+        rg, rp = tm.tilemix_route_coverage(p, words)
+        og, op = coverage(geo, R)
+        assert abs(rg - og) < 1e-12 and abs(rp - op) < 1e-12, (kind, kw, rg, og, rp, op)
+
+
+def test_auto_group_size_matches_oracle():
+    for L in list(range(1, 3000, 29)) + [2 ** k for k in range(6, 19)] + [262144]:
+        for bn in (64, 128):
+            assert tm.tilemix_auto_group_size(L, bn) == auto_group_size(L, bn), (L, bn)
+    assert tm.tilemix_auto_group_size(0, 64) == 0
+
+
+INT_FITS = [("band", "band_w", lambda geo: range(0, geo.T_mask + 1)),
+            ("global", "global_groups", lambda geo: range(0, geo.T_mask + 1)),
+            ("sptrans", "sp_tail", lambda geo: range(0, 129))]
+
+
+@pytest.mark.parametrize("rho", [0.25, 0.5, 0.75])
+def test_fit_integer_parameters_are_optimal(rho):
+    g = GEOMS[0]
+    p, geo = _params(g), _geo(g)
+    for kind, field, rng in INT_FITS:
+        base = tm.Template(kind, sp_stride=128)
+        fit = tm.tilemix_fit_template(p, base, rho)
+        got = coverage(geo, template_map(geo, kind, **{field: getattr(fit, field)},
+                                         **({"sp_stride": 128} if kind == "sptrans" else {})))[0]
+        best = min(abs(coverage(geo, template_map(geo, kind, **{field: v},
+                                                  **({"sp_stride": 128} if kind == "sptrans" else {})))[0] - rho)
+                   for v in rng(geo))
+        assert abs(got - rho) <= best + 1e-12, (kind, rho, got, best)
+
+
+@pytest.mark.parametrize("rho", [0.25, 0.5, 0.75])
+def test_fit_real_parameters(rho):
+    g = GEOMS[0]
+    p, geo = _params(g), _geo(g)
+    fit = tm.tilemix_fit_template(p, tm.Template("rowrand", seed=1), rho)
+    assert abs(fit.rand_fp16 - (1 - rho)) < 1e-6
+    for kind, field, grid in [("aligned", "align_beta", np.linspace(0, geo.T_mask, 161)),
+                              ("bigbird", "rand_fp16", np.linspace(0, 1, 161))]:
+        fit = tm.tilemix_fit_template(p, tm.Template(kind, seed=4), rho)
+        kw = dict(align_alpha=fit.align_alpha, align_beta=fit.align_beta) if kind == "aligned" else \
+            dict(band_w=fit.band_w, global_groups=fit.global_groups, rand_fp16=fit.rand_fp16, seed=4)
+        got = coverage(geo, template_map(geo, kind, **kw))[0]
+        best = 1.0
+        for v in grid:
+            kv = dict(kw, **{field: float(np.float32(v))})
+            best = min(best, abs(coverage(geo, template_map(geo, kind, **kv))[0] - rho))
+        assert abs(got - rho) <= best + 1e-12, (kind, rho, got, best)
+
+
+def test_template_errors():
+    p = _params(GEOMS[0])
+    for bad in (tm.Template("band", band_w=-1), tm.Template("rowrand", rand_fp16=1.5),
+                tm.Template("sptrans", sp_stride=0), tm.Template("bigbird", band_w=-2)):
+        with pytest.raises(tm.TilemixError) as e:
+            tm.tilemix_route_template(p, bad)
+        assert e.value.status == 2
+    with pytest.raises(tm.TilemixError):
+        tm.tilemix_fit_template(p, tm.Template("band"), 1.5)
