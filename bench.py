@@ -153,9 +153,9 @@ def main(argv=None):
         rho = float(rho) if rho else 0.75
         tp = tm.Params(cfg.B, cfg.Hq, cfg.Hk, cfg.L, cfg.L, cfg.d, cfg.block_m, cfg.block_n,
                        cfg.group_size, cfg.causal, cfg.scale)
-        # SpTrans: stride of sqrt(L) tokens rounded to whole key groups
+        # SpTrans: a stride of about sqrt(T_mask) whole key groups
         span = cfg.group_size * cfg.block_n
-        stride = max(span, int(round(math.sqrt(cfg.L) / span)) * span)
+        stride = span * max(1, int(round(math.sqrt(cfg.T_mask))))
         tmpl = tm.tilemix_fit_template(tp, tm.Template(kind, sp_stride=stride, seed=cfg.seed), rho)
         words = tm.tilemix_route_template(tp, tmpl)
         rho_g, rho_p = tm.tilemix_route_coverage(tp, words)

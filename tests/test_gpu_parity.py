@@ -340,3 +340,23 @@ def test_per_sequence_route_maps():
     ref = _oracle(cfg, Q, K, V, words, rows)
     mx, rel = compare_rows(O, rows, ref)
     assert mx <= MAX_ABS and rel <= REL_L2
+
+
+@pytest.mark.parametrize("kind", ["band", "global", "rowrand", "aligned", "bigbird", "sptrans"])
+def test_template_routes_parity(kind):
+    # routing words from the library's Appendix B templates (fitted to 50% INT8 coverage)
+    import paper_2608_17336_amd as tm
+    cfg = small_workload("tmpl", B=1, Hq=4, Hk=2, d=128, L=1300, block_m=128, group_size=2,
+                         k_outliers=True, index=700)
+    p = tm.Params(cfg.B, cfg.Hq, cfg.Hk, cfg.L, cfg.L, cfg.d, cfg.block_m, cfg.block_n,
+                  cfg.group_size, True, cfg.scale)
+    t = tm.tilemix_fit_template(p, tm.Template(kind, sp_stride=256, seed=5), 0.5)
+    words = tm.tilemix_route_template(p, t)
+    log(f"template {t} coverage {tm.tilemix_route_coverage(p, words)}")
+    Q, K, V = make_qkv(cfg)
+    O = prefill(cfg, Q, K, V, words)
+    rows = [(0, h, np.arange(cfg.L)) for h in range(cfg.Hq)]
+    ref = _oracle(cfg, Q, K, V, words, rows)
+    mx, rel = compare_rows(O, rows, ref)
+    log(f"  max_abs={mx:.3e} rel_l2={rel:.3e}")
+    assert mx <= MAX_ABS and rel <= REL_L2, (kind, mx, rel)
