@@ -122,6 +122,9 @@ def main(argv=None):
                          "bigbird, sptrans; RHO the INT8 coverage to fit, default 0.75)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="cap on oracle rows (0 = default sample)")
+    ap.add_argument("--varlen", default="",
+                    help="time a packed variable-length batch instead: comma-separated sequence "
+                         "lengths (the workload's heads, d, tile, g, mask kind and seed)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 256 MiB device copy (HBM counter calibration)")
     args = ap.parse_args(argv)
@@ -143,6 +146,8 @@ def main(argv=None):
     mask = cfg.masks[args.mask]
     dev = torch.device("cuda:0")
     tm.load_library()
+    if args.varlen:
+        return bench_varlen(args, cfg, mask)
 
     t0 = time.perf_counter()
     Q, K, V = make_qkv(cfg)
@@ -277,6 +282,75 @@ def main(argv=None):
         cb = cpu_baseline(cfg, Q, K, V, words, args.cpu_rows or None)
         cb.pop("seconds")
         line["cpu_baseline"] = cb
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def bench_varlen(args, cfg, mask):
+    """One step = tilemix_prefill_varlen over a packed batch of the given sequence lengths
+    (sequence table, quantize-once, V tiles and the fused kernel), causal, with the workload's
+    heads, head size, tile, group size and routing mask kind drawn per sequence."""
+    import numpy as np
+    import torch
+
+    import paper_2608_17336_amd as tm
+    from synth import make_qkv, make_route_bits, route_stats
+
+    lens = [int(x) for x in args.varlen.split(",") if x]
+    dev = torch.device("cuda:0")
+    qs, ks, vs, rows, pairs, int8_pairs = [], [], [], [], 0, 0.0
+    Lmax = max(lens)
+    p = tm.Params(len(lens), cfg.Hq, cfg.Hk, Lmax, Lmax, cfg.d, cfg.block_m, cfg.block_n,
+                  cfg.group_size, True, cfg.scale)
+    W = tm.tilemix_route_words_per_row(p)
+    for i, L in enumerate(lens):
+        c = cfg.with_(B=1, L=L, index=cfg.index * 1000 + i)
+        Q, K, V = make_qkv(c)
+        words, R = make_route_bits(c, mask, args.mask)
+        st = route_stats(c, R)
+        pairs += c.legal_pairs()
+        int8_pairs += c.legal_pairs() * st["rho_pairs"]
+        full = np.zeros((c.Hk, c.T_m, W), np.uint64)
+        full[..., :words.shape[-1]] = words[0]
+        qs.append(Q[0]); ks.append(K[0]); vs.append(V[0]); rows.append(full.transpose(1, 0, 2))
+    to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    q, k, v = to(np.concatenate(qs)), to(np.concatenate(ks)), to(np.concatenate(vs))
+    w = to(np.concatenate(rows).view(np.int64))
+    cu = to(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32))
+    hint = 0 if mask.kind == "all_fp16" else -1
+    ws = torch.empty(tm.tilemix_varlen_workspace_size(p, sum(lens), sum(lens)), dtype=torch.uint8, device=dev)
+    O = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+    run = lambda: tm.tilemix_prefill_varlen(q, k, v, cu, cu, Lmax, Lmax, w, cfg.group_size,
+                                            (cfg.block_m, cfg.block_n), True, cfg.scale, O=O,
+                                            workspace=ws, stream=stream, route_hint=hint)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms = e0.elapsed_time(e1) / args.steps
+    rho = int8_pairs / pairs
+    flops = 4.0 * cfg.d * pairs
+    t_star = (2.0 * cfg.d * pairs * (1 - rho)) / P16 + (2.0 * cfg.d * pairs * rho) / P8 + 2.0 * cfg.d * pairs / P16
+    line = {
+        "metric": METRIC + " (variable-length batch)",
+        "value": round(flops / (wall * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16+i8",
+        "data": "synthetic",
+        "config": {"workload": f"varlen-{cfg.name}", "lens": lens, "Hq": cfg.Hq, "Hk": cfg.Hk,
+                   "d": cfg.d, "tile": f"{cfg.block_m}x{cfg.block_n}", "group_size": cfg.group_size,
+                   "mask": mask.label, "rho_pairs": round(rho, 4)},
+        "step_ms_events": round(ms, 4),
+        "pct_of_weighted_roofline": round(100.0 * t_star / (wall * 1e-3), 2),
+    }
     print(json.dumps(line), flush=True)
     return 0
 

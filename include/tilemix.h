@@ -154,6 +154,36 @@ tilemix_status tilemix_debug_qk_int32(const tilemix_params* params, const int8_t
                                       const int8_t* K8, const int32_t* tiles, int32_t count,
                                       int32_t* out, void* stream);
 
+/* ------------------------------------------------------------ variable-length batching
+ * A batch of B sequences of different lengths, packed without padding (Section 4.1: flattened
+ * inputs with cu_seqlens prefix sums; Appendix C: per-sequence scale blocks).
+ *   params          batch = B; len_q / len_k = the maximum query / key length of any
+ *                   sequence (they size the grid and the routing rows); route_per_batch = 0;
+ *                   every other field as for tilemix_prefill
+ *   total_q/total_k rows of the packed Q / K tensors (>= 1)
+ *   cu_seqlens_q/k  device int32 [B + 1]: sequence b owns Q rows cu_seqlens_q[b] ..
+ *                   cu_seqlens_q[b+1] - 1 and K/V rows cu_seqlens_k[b] .. cu_seqlens_k[b+1] - 1
+ *                   (cu[0] = 0, nondecreasing, lengths within the maxima).  The library reads
+ *                   them only on the device; out-of-range entries are clamped so that every
+ *                   access stays inside the tensors, with unspecified output.
+ *   Q, O            device FP16 [total_q, H_q, d];  K, V device FP16 [total_k, H_k, d]
+ *   route_bits      device uint64 [sum_b ceil(L_q,b / BLOCK_M), H_k, W]: the routing rows of
+ *                   sequence b follow those of sequence b - 1; W = tilemix_route_words_per_row
+ *                   (params), i.e. from the maximum key length; group bits as for
+ *                   tilemix_prefill against that sequence's own legal groups
+ *   workspace       >= tilemix_varlen_workspace_size() bytes, 256-byte aligned
+ * Each sequence is attended on its own: bottom-right causal alignment with its own lengths,
+ * quantization blocks restart at its first row (Appendix C varlen scale layout).
+ */
+tilemix_status tilemix_varlen_workspace_size(const tilemix_params* params, int32_t total_q,
+                                             int32_t total_k, size_t* bytes);
+
+tilemix_status tilemix_prefill_varlen(const tilemix_params* params, int32_t total_q,
+                                      int32_t total_k, const int32_t* cu_seqlens_q,
+                                      const int32_t* cu_seqlens_k, const void* Q, const void* K,
+                                      const void* V, const uint64_t* route_bits, void* O,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------ routing templates
  * Host-side routing policies of Appendix B ("Policy Construction and Sharing", "Coverage
  * Accounting" and the layouts One, Zero, Band, Global, Row-Random, Aligned Sparse, BigBird,
@@ -206,6 +236,14 @@ int32_t tilemix_auto_group_size(int32_t len_k, int32_t block_n);
  * template fields. */
 tilemix_status tilemix_route_template(const tilemix_params* params, const tilemix_template* tmpl,
                                       uint64_t* words);
+
+/* A template for each sequence of a variable-length batch, in the layout
+ * tilemix_prefill_varlen reads: HOST uint64 [sum_b ceil(seqlens_q[b] / BLOCK_M), H_k, W] with
+ * W from params->len_k.  seqlens_q / seqlens_k: HOST int32 [B] lengths, each within
+ * params->len_q / len_k. */
+tilemix_status tilemix_route_template_varlen(const tilemix_params* params, const int32_t* seqlens_q,
+                                             const int32_t* seqlens_k, const tilemix_template* tmpl,
+                                             uint64_t* words);
 
 /* Realized coverage of HOST routing words [B_r, H_k, T_m, W] (Appendix B, "Coverage
  * Accounting"): rho_groups = INT8 share of the legal (h_k, m, g_j) groups; rho_pairs = INT8

@@ -30,8 +30,11 @@ __all__ = [
     "TEMPLATE_KINDS",
     "tilemix_auto_group_size",
     "tilemix_route_template",
+    "tilemix_route_template_varlen",
     "tilemix_route_coverage",
     "tilemix_fit_template",
+    "tilemix_varlen_workspace_size",
+    "tilemix_prefill_varlen",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -45,8 +48,11 @@ EXPORTED_SYMBOLS = (
     "tilemix_debug_qk_int32",
     "tilemix_auto_group_size",
     "tilemix_route_template",
+    "tilemix_route_template_varlen",
     "tilemix_route_coverage",
     "tilemix_fit_template",
+    "tilemix_varlen_workspace_size",
+    "tilemix_prefill_varlen",
     "tilemix_status_string",
     "tilemix_last_error",
 )
@@ -189,6 +195,14 @@ def load_library() -> ctypes.CDLL:
     lib.tilemix_auto_group_size.restype = ctypes.c_int32
     lib.tilemix_route_template.argtypes = [P, TP, vp]
     lib.tilemix_route_template.restype = ctypes.c_int
+    lib.tilemix_route_template_varlen.argtypes = [P, vp, vp, TP, vp]
+    lib.tilemix_route_template_varlen.restype = ctypes.c_int
+    lib.tilemix_varlen_workspace_size.argtypes = [P, ctypes.c_int32, ctypes.c_int32,
+                                                  ctypes.POINTER(ctypes.c_size_t)]
+    lib.tilemix_varlen_workspace_size.restype = ctypes.c_int
+    lib.tilemix_prefill_varlen.argtypes = [P, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp, vp, vp,
+                                           vp, vp, ctypes.c_size_t, vp]
+    lib.tilemix_prefill_varlen.restype = ctypes.c_int
     lib.tilemix_route_coverage.argtypes = [P, vp, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_double)]
     lib.tilemix_route_coverage.restype = ctypes.c_int
@@ -402,3 +416,64 @@ def tilemix_fit_template(params: Params, template: Template, rho_int8: float) ->
     _check(load_library().tilemix_fit_template(ctypes.byref(cp), ctypes.byref(ct),
                                                ctypes.c_double(rho_int8)))
     return Template.from_c(template.kind, ct)
+
+
+def tilemix_route_template_varlen(params: Params, seqlens_q, seqlens_k, template: Template):
+    """Routing words (host uint64 [sum_b ceil(L_q,b / BLOCK_M), H_k, W]) of ``template`` for each
+    sequence of a variable-length batch (``params.len_q``/``len_k`` = maximum lengths)."""
+    import numpy as np
+    lq = np.ascontiguousarray(seqlens_q, dtype=np.int32)
+    lk = np.ascontiguousarray(seqlens_k, dtype=np.int32)
+    if lq.shape != (params.batch,) or lk.shape != (params.batch,):
+        raise ValueError("seqlens_q / seqlens_k must have one entry per sequence")
+    rows = int(sum(-(-int(x) // params.block_m) for x in lq))
+    words = np.zeros((rows, params.heads_kv, tilemix_route_words_per_row(params)), dtype=np.uint64)
+    cp, ct = params.c(), template.c()
+    _check(load_library().tilemix_route_template_varlen(
+        ctypes.byref(cp), lq.ctypes.data_as(ctypes.c_void_p), lk.ctypes.data_as(ctypes.c_void_p),
+        ctypes.byref(ct), words.ctypes.data_as(ctypes.c_void_p)))
+    return words
+
+
+def tilemix_varlen_workspace_size(params: Params, total_q: int, total_k: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().tilemix_varlen_workspace_size(ctypes.byref(params.c()), total_q, total_k,
+                                                        ctypes.byref(n)))
+    return int(n.value)
+
+
+def tilemix_prefill_varlen(Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q: int, max_len_k: int,
+                           route_bits, group_size: int, tile=(128, 64), causal: bool = True,
+                           scale: float | None = None, *, O=None, workspace=None, stream=None,
+                           route_hint: int = -1):
+    """Routed prefill attention over a packed variable-length batch.  Q [total_q, Hq, d],
+    K/V [total_k, Hk, d] fp16 CUDA tensors; cu_seqlens_q/k int32 CUDA [B + 1]; route_bits the
+    uint64 words [sum_b ceil(L_q,b / BLOCK_M), Hk, W] as an int64 CUDA tensor.  Returns O."""
+    import torch
+    total_q, Hq, d = Q.shape
+    total_k, Hk = K.shape[0], K.shape[1]
+    B = cu_seqlens_q.shape[0] - 1
+    p = Params(B, Hq, Hk, max_len_q, max_len_k, d, tile[0], tile[1], group_size, causal,
+               scale if scale else 1.0 / math.sqrt(d), False, route_hint)
+    _require(Q, torch.float16, (total_q, Hq, d), "Q")
+    _require(K, torch.float16, (total_k, Hk, d), "K")
+    _require(V, torch.float16, (total_k, Hk, d), "V")
+    _require(cu_seqlens_q, torch.int32, (B + 1,), "cu_seqlens_q")
+    _require(cu_seqlens_k, torch.int32, (B + 1,), "cu_seqlens_k")
+    if route_bits.dim() != 3 or tuple(route_bits.shape[1:]) != (Hk, tilemix_route_words_per_row(p)):
+        raise ValueError("route_bits must be [rows, H_k, W]")
+    _require(route_bits, torch.int64, tuple(route_bits.shape), "route_bits")
+    if O is None:
+        O = torch.empty((total_q, Hq, d), dtype=torch.float16, device=Q.device)
+    _require(O, torch.float16, (total_q, Hq, d), "O")
+    need = tilemix_varlen_workspace_size(p, total_q, total_k)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=Q.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    if nbytes < need:
+        raise ValueError(f"workspace too small: {need} bytes needed")
+    cp = p.c()
+    _check(load_library().tilemix_prefill_varlen(
+        ctypes.byref(cp), total_q, total_k, _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), _ptr(Q), _ptr(K),
+        _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace), ctypes.c_size_t(nbytes), _stream(stream)))
+    return O

@@ -354,6 +354,26 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
 
   int b, hq0, hk, m;
   decode_unit<HEADS>(blockIdx.x, a.B, a.Hq, a.Hk, a.T_m, b, hq0, hk, m);
+  // This sequence: its lengths, first rows in Q and K, first scale blocks, and the addresses
+  // of this routing row and of this KV head's first V tile.
+  int Lq = a.Lq, Lk = a.Lk;
+  long long q_row0 = (long long)b * a.Lq, k_row0 = (long long)b * a.Lk;
+  long long qblk0 = (long long)b * a.nQB, kblk0 = (long long)b * a.nKB;
+  const uint64_t* route_row =
+      a.route + (size_t)b * a.route_batch_stride + ((size_t)hk * a.T_m + m) * a.W;
+  long long vt_tile0 = ((long long)b * a.Hk + hk) * a.T_n;
+  if (a.seqs) {
+    const int* e = a.seqs + kSeqFields * b;
+    Lq = e[kSeqQLen];
+    Lk = e[kSeqKLen];
+    if (m * BM >= Lq) return;   // past the end of a shorter sequence: no rows to write
+    q_row0 = e[kSeqQStart];
+    k_row0 = e[kSeqKStart];
+    qblk0 = e[kSeqQBlk];
+    kblk0 = e[kSeqKBlk];
+    route_row = a.route + ((size_t)(e[kSeqQTile] + m) * a.Hk + hk) * a.W;
+    vt_tile0 = (long long)hk * a.seqs[kSeqFields * a.B + kSeqKTile] + e[kSeqKTile];
+  }
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -365,17 +385,17 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   const int my_q = q0 + lq;
   // Row i may see keys j <= i + off (bottom-right causal alignment); without the causal
   // mask every key up to L_k - 1 is legal.
-  const int off = a.causal ? a.Lk - a.Lq : a.Lk;
-  const bool wave_active = q0 < a.Lq;
+  const int off = a.causal ? Lk - Lq : Lk;
+  const bool wave_active = q0 < Lq;
 
   // Last key any row of the workgroup / of this wave may see.
-  const int wg_last_key = min(a.Lk - 1, min(a.Lq - 1, m * BM + BM - 1) + off);
-  const int wave_last_key = min(a.Lk - 1, min(a.Lq - 1, q0 + 31) + off);
-  const int my_last_key = min(a.Lk - 1, my_q + off);
+  const int wg_last_key = min(Lk - 1, min(Lq - 1, m * BM + BM - 1) + off);
+  const int wave_last_key = min(Lk - 1, min(Lq - 1, q0 + 31) + off);
+  const int my_last_key = min(Lk - 1, my_q + off);
 
-  _Float16* orow = a.O + (((size_t)b * a.Lq + my_q) * a.Hq + hq) * D;
+  _Float16* orow = a.O + ((size_t)(q_row0 + my_q) * a.Hq + hq) * D;
   if (wg_last_key < 0) {   // no legal key for any row of this tile: output is zero
-    if (my_q < a.Lq) {     // the two lanes of a row each clear half of it
+    if (my_q < Lq) {       // the two lanes of a row each clear half of it
 #pragma unroll
       for (int c = 0; c < D / 2; c += 8) *reinterpret_cast<half8*>(orow + hi * (D / 2) + c) = half8{};
     }
@@ -385,8 +405,6 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
 
   // Routing words of this row: lane w holds word w (at most 64 words per row), so the
   // per-tile lookup is a lane read plus a shift-and-mask, with no memory access in the loop.
-  const uint64_t* route_row =
-      a.route + (size_t)b * a.route_batch_stride + ((size_t)hk * a.T_m + m) * a.W;
   const uint64_t my_word = (!a.force_fp16 && lane < a.W) ? route_row[lane] : 0ull;
   const uint32_t word_lo = (uint32_t)my_word, word_hi = (uint32_t)(my_word >> 32);
   auto group_route = [&](int gj) -> bool {   // routing bit of tile group gj
@@ -409,8 +427,8 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   // Q operands of this wave, kept in registers for the whole row.
   half8 qf[D / 16];
   i32x4 q8f[D / 32];
-  const bool row_ok = my_q < a.Lq;
-  const size_t qoff = (((size_t)b * a.Lq + (row_ok ? my_q : 0)) * a.Hq + hq) * D;
+  const bool row_ok = my_q < Lq;
+  const size_t qoff = ((size_t)(q_row0 + (row_ok ? my_q : 0)) * a.Hq + hq) * D;
 #pragma unroll
   for (int s = 0; s < D / 16; ++s)
     qf[s] = (need_fp16 && row_ok) ? as_half8(ld_global_16(a.Q + qoff + 16 * s + 8 * hi)) : half8{};
@@ -418,21 +436,20 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   for (int s = 0; s < D / 32; ++s)
     q8f[s] = (need_int8 && row_ok) ? as_i32x4(ld_global_16(a.Q8 + qoff + 32 * s + 16 * hi)) : i32x4{};
   const float dq = (need_int8 && wave_active)
-                       ? load_scale_uniform(a.dQ, ((size_t)b * a.nQB + q0 / kQuantBlockQ) * a.Hq + hq)
+                       ? load_scale_uniform(a.dQ, (size_t)(qblk0 + q0 / kQuantBlockQ) * a.Hq + hq)
                        : 0.0f;
   const float c_fp16 = a.scale_log2e;
   const float c_int8_q = a.scale_log2e * dq;
   if (need_int8) {   // key-block scales of the tiles this row visits (key block = key tile)
     for (int t = tid; t <= n_end; t += C::kThreads)
-      key_scale[t] = a.dK[((size_t)b * a.nKB + t) * a.Hk + hk];
+      key_scale[t] = a.dK[(size_t)(kblk0 + t) * a.Hk + hk];
   }
 
   // Tile sources (uniform bases) and per-lane LDS fragment offsets.
   const int kstride = a.Hk * D * 2;                              // bytes between keys (FP16)
-  const char* kbase = reinterpret_cast<const char*>(a.K) + ((size_t)b * a.Lk * a.Hk + hk) * D * 2;
-  const char* k8base = reinterpret_cast<const char*>(a.K8) + ((size_t)b * a.Lk * a.Hk + hk) * D;
-  const char* vbase = reinterpret_cast<const char*>(a.Vt) +
-                      ((size_t)b * a.Hk + hk) * a.T_n * (size_t)(D * kBlockN * 2);
+  const char* kbase = reinterpret_cast<const char*>(a.K) + ((size_t)k_row0 * a.Hk + hk) * D * 2;
+  const char* k8base = reinterpret_cast<const char*>(a.K8) + ((size_t)k_row0 * a.Hk + hk) * D;
+  const char* vbase = reinterpret_cast<const char*>(a.Vt) + (size_t)vt_tile0 * (size_t)(D * kBlockN * 2);
   const DmaPlan<C::kKRow> plan_k(lane, kstride);
   const DmaPlan<C::kK8Row> plan_k8(lane, kstride / 2);
   const DmaPlan<C::kVRow> plan_v(lane, C::kVRow);
@@ -454,7 +471,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     const uint64_t bit = 1ull << (iss_kt & 63);
     route_ring = int8 ? (route_ring | bit) : (route_ring & ~bit);
     const uint32_t dst = smem_lds + (uint32_t)k_slot(iss_kt);
-    const int rows = min(kBlockN, a.Lk - iss_kt * kBlockN);
+    const int rows = min(kBlockN, Lk - iss_kt * kBlockN);
     if (int8)
       dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(iss_k8, kstride / 2, rows, dst, wave, lane, plan_k8);
     else   // 8 copies per 64-channel half of the FP16 key tile
@@ -669,7 +686,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   using QKInt8Exact = std::integral_constant<int, 3>;
 
   // Tiles whose every key every row of the workgroup may see: keys <= the first row's last key.
-  const int wg_first_row_last_key = min(a.Lk - 1, m * BM + off);
+  const int wg_first_row_last_key = min(Lk - 1, m * BM + off);
   const int n_split = max(0, min(n_end + 1, (wg_first_row_last_key + 1) / kBlockN));
 
   issue(1, 0);   // K of tiles 0 and 1, V of tile 0

@@ -27,8 +27,12 @@ using tilemix::api::ok;
 struct Geometry {
   long long Lq, Lk, BM, BN, g, span, T_m, T_mask, W, off;
   bool causal;
-  explicit Geometry(const tilemix_params& p) {
-    Lq = p.len_q; Lk = p.len_k; BM = p.block_m; BN = p.block_n; g = p.group_size;
+  // Lengths default to the params' (one sequence); a sequence of a variable-length batch
+  // passes its own.
+  explicit Geometry(const tilemix_params& p, long long len_q = -1, long long len_k = -1) {
+    Lq = len_q >= 0 ? len_q : p.len_q;
+    Lk = len_k >= 0 ? len_k : p.len_k;
+    BM = p.block_m; BN = p.block_n; g = p.group_size;
     span = g * BN;
     T_m = (Lq + BM - 1) / BM;
     T_mask = ((Lk + BN - 1) / BN + g - 1) / g;
@@ -211,6 +215,34 @@ tilemix_status tilemix_route_template(const tilemix_params* params, const tilemi
   const long long planes = (long long)(params->route_per_batch ? params->batch : 1) * params->heads_kv;
   for (long long h = 0; h < planes; ++h)
     memcpy(words + (size_t)h * plane.size(), plane.data(), plane.size() * sizeof(uint64_t));
+  return ok();
+}
+
+tilemix_status tilemix_route_template_varlen(const tilemix_params* params, const int32_t* seqlens_q,
+                                             const int32_t* seqlens_k, const tilemix_template* tmpl,
+                                             uint64_t* words) {
+  tilemix_status st = tilemix::api::validate(params);
+  if (st != TILEMIX_OK) return st;
+  if ((st = check_template(tmpl)) != TILEMIX_OK) return st;
+  if (!words || !seqlens_q || !seqlens_k) return fail(TILEMIX_ERR_NULL, "NULL pointer");
+  const long long W = Geometry(*params).W;   // words per row of the longest key sequence
+  std::vector<uint8_t> f;
+  uint64_t* out = words;
+  for (int b = 0; b < params->batch; ++b) {
+    if (seqlens_q[b] < 0 || seqlens_q[b] > params->len_q || seqlens_k[b] < 0 ||
+        seqlens_k[b] > params->len_k)
+      return fail(TILEMIX_ERR_SHAPE, "sequence %d has lengths (%d, %d) outside [0, (%d, %d)]", b,
+                  seqlens_q[b], seqlens_k[b], params->len_q, params->len_k);
+    const Geometry G(*params, seqlens_q[b], seqlens_k[b]);
+    f.assign((size_t)std::max(1LL, G.T_mask), 0);
+    for (long long m = 0; m < G.T_m; ++m) {
+      fp16_row(G, *tmpl, m, f);
+      std::vector<uint64_t> row((size_t)W, 0ull);
+      for (long long x = 0; x <= G.gmax(m); ++x)
+        if (!f[x]) row[x >> 6] |= 1ull << (x & 63);
+      for (int h = 0; h < params->heads_kv; ++h, out += W) memcpy(out, row.data(), W * sizeof(uint64_t));
+    }
+  }
   return ok();
 }
 

@@ -83,15 +83,17 @@ using tilemix::api::validate;
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
-// Derived sizes of one problem.
+// Derived sizes of one problem.  A variable-length batch (total_q >= 0) sizes its buffers by
+// the packed row counts: B sequences of total_q / total_k rows hold at most total / block + B
+// blocks or tiles, and its workspace starts with the device-built sequence table.
 struct Plan {
   long long T_m, T_n, T_mask, W;
   long long nQB, nKB;
-  size_t q8_bytes, k8_bytes, dq_bytes, dk_bytes, vt_bytes;
-  size_t q8_off, k8_off, dq_off, dk_off, vt_off, total;
+  size_t seq_bytes, q8_bytes, k8_bytes, dq_bytes, dk_bytes, vt_bytes;
+  size_t seq_off, q8_off, k8_off, dq_off, dk_off, vt_off, total;
 };
 
-Plan make_plan(const tilemix_params* p) {
+Plan make_plan(const tilemix_params* p, long long total_q = -1, long long total_k = -1) {
   Plan pl{};
   pl.T_m = cdiv(p->len_q, p->block_m);
   pl.T_n = cdiv(p->len_k, p->block_n);
@@ -100,12 +102,20 @@ Plan make_plan(const tilemix_params* p) {
   pl.nQB = cdiv(p->len_q, tilemix::kQuantBlockQ);
   pl.nKB = cdiv(p->len_k, tilemix::kQuantBlockK);
   const size_t d = (size_t)p->head_dim;
-  pl.q8_bytes = (size_t)p->batch * p->len_q * p->heads_q * d;
-  pl.k8_bytes = (size_t)p->batch * p->len_k * p->heads_kv * d;
-  pl.dq_bytes = (size_t)p->batch * pl.nQB * p->heads_q * 2;
-  pl.dk_bytes = (size_t)p->batch * pl.nKB * p->heads_kv * 2;
-  pl.vt_bytes = (size_t)p->batch * p->heads_kv * pl.T_n * d * tilemix::kBlockN * 2;
-  pl.q8_off = 0;
+  const bool varlen = total_q >= 0;
+  const long long rows_q = varlen ? total_q : (long long)p->batch * p->len_q;
+  const long long rows_k = varlen ? total_k : (long long)p->batch * p->len_k;
+  const long long qblocks = varlen ? cdiv(total_q, tilemix::kQuantBlockQ) + p->batch : p->batch * pl.nQB;
+  const long long kblocks = varlen ? cdiv(total_k, tilemix::kQuantBlockK) + p->batch : p->batch * pl.nKB;
+  const long long ktiles = varlen ? cdiv(total_k, tilemix::kBlockN) + p->batch : p->batch * pl.T_n;
+  pl.seq_bytes = varlen ? (size_t)(p->batch + 1) * tilemix::kSeqFields * sizeof(int) : 0;
+  pl.q8_bytes = (size_t)rows_q * p->heads_q * d;
+  pl.k8_bytes = (size_t)rows_k * p->heads_kv * d;
+  pl.dq_bytes = (size_t)qblocks * p->heads_q * 2;
+  pl.dk_bytes = (size_t)kblocks * p->heads_kv * 2;
+  pl.vt_bytes = (size_t)ktiles * p->heads_kv * d * tilemix::kBlockN * 2;
+  pl.seq_off = 0;
+  pl.q8_off = align256(pl.seq_off + pl.seq_bytes);
   pl.k8_off = align256(pl.q8_off + pl.q8_bytes);
   pl.dq_off = align256(pl.k8_off + pl.k8_bytes);
   pl.dk_off = align256(pl.dq_off + pl.dq_bytes);
@@ -148,8 +158,10 @@ tilemix_status check_workspace(const Plan& pl, const void* workspace, size_t wor
   return TILEMIX_OK;
 }
 
+// seqs: the sequence table of a variable-length batch (in the workspace), or nullptr.
 tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void* Q, const void* K,
-                            const void* V, void* workspace, hipStream_t s) {
+                            const void* V, void* workspace, hipStream_t s,
+                            const int* seqs = nullptr) {
   char* ws = static_cast<char*>(workspace);
   int8_t* q8 = reinterpret_cast<int8_t*>(ws + pl.q8_off);
   int8_t* k8 = reinterpret_cast<int8_t*>(ws + pl.k8_off);
@@ -160,22 +172,23 @@ tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void*
   if (p.route_hint != 0) {   // an all-FP16 map skips the quantize-once pass
     st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(Q), q8, dq, p.batch,
                                              p.len_q, p.heads_q, p.head_dim,
-                                             tilemix::kQuantBlockQ, s), "quantize Q");
+                                             tilemix::kQuantBlockQ, seqs, false, s), "quantize Q");
     if (st != TILEMIX_OK) return st;
     st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(K), k8, dk, p.batch,
                                              p.len_k, p.heads_kv, p.head_dim,
-                                             tilemix::kQuantBlockK, s), "quantize K");
+                                             tilemix::kQuantBlockK, seqs, true, s), "quantize K");
     if (st != TILEMIX_OK) return st;
   }
   return hip_status(tilemix::launch_v_tiles(static_cast<const _Float16*>(V), vt, p.batch, p.len_k,
-                                            p.heads_kv, p.head_dim, s), "V tiles");
+                                            p.heads_kv, p.head_dim, seqs, s), "V tiles");
 }
 
 tilemix_status attend_impl(const tilemix_params& p, const Plan& pl, const void* Q, const void* K,
                            const uint64_t* route_bits, void* O, const void* workspace,
-                           hipStream_t s) {
+                           hipStream_t s, const int* seqs = nullptr) {
   const char* ws = static_cast<const char*>(workspace);
   tilemix::AttnArgs a{};
+  a.seqs = seqs;
   a.Q = static_cast<const _Float16*>(Q);
   a.K = static_cast<const _Float16*>(K);
   a.Vt = reinterpret_cast<const _Float16*>(ws + pl.vt_off);
@@ -254,6 +267,56 @@ tilemix_status tilemix_attend(const tilemix_params* params, const void* Q, const
   return ok();
 }
 
+namespace {
+
+tilemix_status check_varlen(const tilemix_params* params, int32_t total_q, int32_t total_k) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  if (total_q < 1 || total_k < 1) return fail(TILEMIX_ERR_SHAPE, "total_q and total_k must be >= 1");
+  if (params->route_per_batch != 0)
+    return fail(TILEMIX_ERR_SHAPE, "route_per_batch must be 0 for a variable-length batch");
+  if ((long long)total_q * params->heads_q * params->head_dim > (1LL << 40) ||
+      (long long)total_k * params->heads_kv * params->head_dim > (1LL << 40))
+    return fail(TILEMIX_ERR_SHAPE, "tensor too large");
+  return TILEMIX_OK;
+}
+
+}  // namespace
+
+tilemix_status tilemix_varlen_workspace_size(const tilemix_params* params, int32_t total_q,
+                                             int32_t total_k, size_t* bytes) {
+  tilemix_status st = check_varlen(params, total_q, total_k);
+  if (st != TILEMIX_OK) return st;
+  if (!bytes) return fail(TILEMIX_ERR_NULL, "bytes is NULL");
+  *bytes = make_plan(params, total_q, total_k).total;
+  return ok();
+}
+
+tilemix_status tilemix_prefill_varlen(const tilemix_params* params, int32_t total_q,
+                                      int32_t total_k, const int32_t* cu_seqlens_q,
+                                      const int32_t* cu_seqlens_k, const void* Q, const void* K,
+                                      const void* V, const uint64_t* route_bits, void* O,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
+  tilemix_status st = check_varlen(params, total_q, total_k);
+  if (st != TILEMIX_OK) return st;
+  if (!cu_seqlens_q || !cu_seqlens_k) return fail(TILEMIX_ERR_NULL, "cu_seqlens must be non-NULL");
+  if (!aligned(cu_seqlens_q, 4) || !aligned(cu_seqlens_k, 4))
+    return fail(TILEMIX_ERR_ALIGN, "cu_seqlens must be 4-byte aligned");
+  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
+  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
+  const Plan pl = make_plan(params, total_q, total_k);
+  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int* seqs = reinterpret_cast<int*>(static_cast<char*>(workspace) + pl.seq_off);
+  st = hip_status(tilemix::launch_seq_table(cu_seqlens_q, cu_seqlens_k, params->batch, total_q,
+                                            total_k, params->len_q, params->len_k,
+                                            params->block_m, seqs, s), "sequence table");
+  if (st != TILEMIX_OK) return st;
+  if ((st = prepare_impl(*params, pl, Q, K, V, workspace, s, seqs)) != TILEMIX_OK) return st;
+  if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, s, seqs)) != TILEMIX_OK) return st;
+  return ok();
+}
+
 tilemix_status tilemix_quantize(const tilemix_params* params, const void* Q, const void* K,
                                 int8_t* Q8, uint16_t* dQ, int8_t* K8, uint16_t* dK, void* stream) {
   tilemix_status st = validate(params);
@@ -265,11 +328,13 @@ tilemix_status tilemix_quantize(const tilemix_params* params, const void* Q, con
     return fail(TILEMIX_ERR_ALIGN, "Q, K, Q8, K8 must be 16-byte and dQ, dK 2-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(Q), Q8, dQ, p.batch, p.len_q,
-                                           p.heads_q, p.head_dim, tilemix::kQuantBlockQ, s),
+                                           p.heads_q, p.head_dim, tilemix::kQuantBlockQ, nullptr,
+                                           false, s),
                   "quantize Q");
   if (st != TILEMIX_OK) return st;
   st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(K), K8, dK, p.batch, p.len_k,
-                                           p.heads_kv, p.head_dim, tilemix::kQuantBlockK, s),
+                                           p.heads_kv, p.head_dim, tilemix::kQuantBlockK, nullptr,
+                                           true, s),
                   "quantize K");
   if (st != TILEMIX_OK) return st;
   return ok();

@@ -19,6 +19,13 @@ const char* last_error();
 tilemix_status validate(const tilemix_params* p);
 }  // namespace api
 
+// Sequence table of a variable-length batch: int32 [B + 1][kSeqFields], row b = sequence b,
+// row B = totals (first free row of Q and K, and the total numbers of Q / K scale blocks,
+// query-tile rows and key tiles).
+constexpr int kSeqFields = 8;
+constexpr int kSeqQStart = 0, kSeqQLen = 1, kSeqKStart = 2, kSeqKLen = 3;
+constexpr int kSeqQBlk = 4, kSeqKBlk = 5, kSeqQTile = 6, kSeqKTile = 7;
+
 // Arguments of the fused routed attention kernel (plain values; passed by value).
 struct AttnArgs {
   const _Float16* Q;      // [B, Lq, Hq, d]
@@ -30,6 +37,11 @@ struct AttnArgs {
   const uint16_t* dK;     // FP16 bits [B, nKB, Hk]
   const uint64_t* route;  // [B_r, Hk, T_m, W]
   _Float16* O;            // [B, Lq, Hq, d]
+  // Variable-length batch: sequence table (see kSeqFields), or nullptr when every sequence has
+  // the lengths Lq / Lk.  With a table, Lq / Lk are the maximum lengths, Q/K/V/O/Q8/K8 are
+  // packed [rows, H, d], scales [blocks, H], V tiles [Hk, key tiles, d, 64] and routing rows
+  // [query-tile rows, Hk, W].
+  const int* seqs;
   int B, Hq, Hk, Lq, Lk;
   int T_m, T_n, W, g;
   int nQB, nKB;
@@ -49,10 +61,13 @@ struct DebugTileArgs {
   int B, Hq, Hk, Lq, Lk;
 };
 
+// seqs: sequence table or nullptr (every sequence of length L); keys selects its K fields.
 hipError_t launch_quantize(const _Float16* X, int8_t* X8, uint16_t* dX, int B, int L, int H,
-                           int d, int block_rows, hipStream_t stream);
+                           int d, int block_rows, const int* seqs, bool keys, hipStream_t stream);
 hipError_t launch_v_tiles(const _Float16* V, _Float16* Vt, int B, int L, int H, int d,
-                          hipStream_t stream);
+                          const int* seqs, hipStream_t stream);
+hipError_t launch_seq_table(const int* cu_q, const int* cu_k, int batch, int total_q, int total_k,
+                            int max_q, int max_k, int block_m, int* seqs, hipStream_t stream);
 hipError_t launch_routed_attention(const AttnArgs& args, int d, int block_m, hipStream_t stream);
 hipError_t launch_debug_tiles(const DebugTileArgs& args, int d, int block_m, hipStream_t stream);
 

@@ -117,3 +117,26 @@ def test_template_errors():
         assert e.value.status == 2
     with pytest.raises(tm.TilemixError):
         tm.tilemix_fit_template(p, tm.Template("band"), 1.5)
+
+
+def test_varlen_templates_match_oracle_per_sequence():
+    lens_q = [300, 0, 517, 64, 1, 129]
+    lens_k = [300, 0, 517, 64, 1, 200]
+    Lq, Lk = max(lens_q), max(lens_k)
+    p = tm.Params(len(lens_q), 4, 2, Lq, Lk, 128, 128, 64, 2, True, 0.0884)
+    W = tm.tilemix_route_words_per_row(p)
+    for kind, kw in TEMPLATES[:12]:
+        words = tm.tilemix_route_template_varlen(p, lens_q, lens_k, tm.Template(kind, **kw))
+        row = 0
+        for lq, lk in zip(lens_q, lens_k):
+            tq = -(-lq // 128)
+            if tq:
+                geo = Geometry(lq, lk, 128, 64, 2, True)
+                want = pack_words(template_map(geo, kind, **kw), 2)[0]       # [H_k, T_m, W_b]
+                got = words[row:row + tq].transpose(1, 0, 2)                 # [H_k, T_m, W]
+                np.testing.assert_array_equal(got[..., :want.shape[-1]], want, err_msg=f"{kind} {lq}")
+                assert not got[..., want.shape[-1]:].any()
+            row += tq
+        assert row == words.shape[0] and words.shape[2] == W
+    with pytest.raises(tm.TilemixError):
+        tm.tilemix_route_template_varlen(p, [Lq + 1] + lens_q[1:], lens_k, tm.Template("one"))
