@@ -125,6 +125,9 @@ def main(argv=None):
     ap.add_argument("--varlen", default="",
                     help="time a packed variable-length batch instead: comma-separated sequence "
                          "lengths (the workload's heads, d, tile, g, mask kind and seed)")
+    ap.add_argument("--decode", action="store_true",
+                    help="time one decode step over an INT8 key/value cache of the workload's "
+                         "shape (L_k = L, one query token per sequence)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 256 MiB device copy (HBM counter calibration)")
     args = ap.parse_args(argv)
@@ -148,6 +151,8 @@ def main(argv=None):
     tm.load_library()
     if args.varlen:
         return bench_varlen(args, cfg, mask)
+    if args.decode:
+        return bench_decode(args, cfg, mask)
 
     t0 = time.perf_counter()
     Q, K, V = make_qkv(cfg)
@@ -282,6 +287,79 @@ def main(argv=None):
         cb = cpu_baseline(cfg, Q, K, V, words, args.cpu_rows or None)
         cb.pop("seconds")
         line["cpu_baseline"] = cb
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def bench_decode(args, cfg, mask):
+    """One step = tilemix_decode: each sequence's newest token against an INT8 key/value cache
+    of L keys (K8 + V8 + scales, and the FP16 key cache for FP16-routed groups).  HBM-bound:
+    the roofline is algorithmic bytes (cache bytes each routed key needs) per launch time."""
+    import numpy as np
+    import torch
+
+    import paper_2608_17336_amd as tm
+    from synth import make_qkv
+
+    dev = torch.device("cuda:0")
+    Q, K, V = make_qkv(cfg)
+    to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    q1, k, v = to(Q[:, -1:]), to(K), to(V)
+    del Q
+    K8, dK, V8, dV = tm.tilemix_quantize_kv(k, v)
+    T_mask = -(-(-(-cfg.L // cfg.block_n)) // cfg.group_size)
+    rng = np.random.default_rng(cfg.seed)
+    if mask.kind == "all_fp16":
+        R = np.zeros((cfg.Hk, 1, T_mask), np.uint8)
+    elif mask.kind == "all_int8":
+        R = np.ones((cfg.Hk, 1, T_mask), np.uint8)
+    else:
+        R = (rng.random((cfg.Hk, 1, T_mask)) < (mask.p_int8 or 0.5)).astype(np.uint8)
+    from synth import pack_route_bits
+    words = pack_route_bits(R)
+    w = to(words.view(np.int64))
+    hint = 0 if mask.kind == "all_fp16" else -1
+    p = tm.Params(cfg.B, cfg.Hq, cfg.Hk, 1, cfg.L, cfg.d, cfg.block_m, cfg.block_n,
+                  cfg.group_size, True, cfg.scale, False, hint)
+    ws = torch.empty(tm.tilemix_decode_workspace_size(p), dtype=torch.uint8, device=dev)
+    O = torch.empty_like(q1)
+    stream = torch.cuda.current_stream()
+    run = lambda: tm.tilemix_decode(q1, k, K8, dK, V8, dV, w, cfg.group_size, cfg.scale, O=O,
+                                    workspace=ws, stream=stream, route_hint=hint)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms = e0.elapsed_time(e1) / args.steps
+    # algorithmic bytes: per KV head and key, d (K8) or 2d (FP16 K) by route, plus d (V8)
+    keys = np.arange(cfg.L)
+    bits = R[:, 0, (keys // cfg.block_n) // cfg.group_size].astype(np.int64)   # [Hk, L]
+    kbytes = float(np.where(bits == 1, cfg.d, 2 * cfg.d).sum()) * cfg.B
+    vbytes = float(cfg.d) * cfg.L * cfg.Hk * cfg.B
+    nkb = -(-cfg.L // 64)
+    sbytes = 2.0 * 2 * nkb * cfg.Hk * cfg.B
+    qo = 2.0 * 2 * cfg.B * cfg.Hq * cfg.d
+    nbytes = kbytes + vbytes + sbytes + qo
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    line = {
+        "metric": "decode step ms over an INT8 key/value cache; % of HBM roofline",
+        "value": round(ms, 4), "unit": "ms", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(wall, 4), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "i8+f16", "data": "synthetic",
+        "config": {"workload": f"decode-{cfg.name}", "B": cfg.B, "Hq": cfg.Hq, "Hk": cfg.Hk,
+                   "d": cfg.d, "L_k": cfg.L, "group_size": cfg.group_size, "mask": mask.label,
+                   "int8_key_share": round(float(bits.mean()), 4)},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": 8000.0, "unit": "GB/s",
+                     "frac": round(gbs / 8000.0, 4), "traffic": None,
+                     "kernel": "decode_partial_kernel + decode_combine_kernel (event-timed step)"},
+    }
     print(json.dumps(line), flush=True)
     return 0
 

@@ -184,6 +184,43 @@ tilemix_status tilemix_prefill_varlen(const tilemix_params* params, int32_t tota
                                       const void* V, const uint64_t* route_bits, void* O,
                                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* --------------------------------------------------------------- INT8 key/value cache decode
+ * Appendix C, "Additional Execution Interfaces": an INT8 key/value cache holds K8 and V8 with
+ * FP16 per-block scales (64-token key blocks per KV head, the key quantization of Appendix C
+ * applied to K and to V).  During decode, cached K8 takes the INT8 score path; cached V8 is
+ * widened on chip with its block scale folded into the probabilities before P.V.
+ *
+ * tilemix_quantize_kv -- build the cache: K8/V8 int8 [B, L_k, H_k, d] and dK/dV FP16 bits
+ * [B, ceil(L_k/64), H_k] from device FP16 K, V [B, L_k, H_k, d] (same rules as
+ * tilemix_quantize).  K8, V8 16-byte and dK, dV 2-byte aligned.
+ */
+tilemix_status tilemix_quantize_kv(const tilemix_params* params, const void* K, const void* V,
+                                   int8_t* K8, uint16_t* dK, int8_t* V8, uint16_t* dV,
+                                   void* stream);
+
+/* Bytes of device workspace tilemix_decode needs (per-chunk partial results), 256-aligned. */
+tilemix_status tilemix_decode_workspace_size(const tilemix_params* params, size_t* bytes);
+
+/*
+ * tilemix_decode -- one decode step: each sequence's newest query token attends to all L_k
+ * cached keys (the last query row of causal attention).
+ *   params      len_q = 1 (one token), len_k = cached keys, H_q / H_k <= 16, block_n = 64, g,
+ *               scale, route_per_batch, route_hint as for tilemix_prefill (block_m is unused:
+ *               the routing rows hold one query-tile row, T_m = 1)
+ *   Q, O        device FP16 [B, 1, H_q, d]
+ *   K           device FP16 key cache [B, L_k, H_k, d], read for FP16-routed groups
+ *   K8, dK      device INT8 key cache and scales (tilemix_quantize_kv), INT8-routed groups
+ *   V8, dV      device INT8 value cache and scales
+ *   route_bits  device uint64 [B_r, H_k, 1, W]
+ *   workspace   >= tilemix_decode_workspace_size() bytes, 256-byte aligned
+ * Scores follow tilemix_prefill (the query's INT8 codes use its own row as the block); the
+ * output is O = sum_j P_j (dV_j V8_j) / sum_j P_j.
+ */
+tilemix_status tilemix_decode(const tilemix_params* params, const void* Q, const void* K,
+                              const int8_t* K8, const uint16_t* dK, const int8_t* V8,
+                              const uint16_t* dV, const uint64_t* route_bits, void* O,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------ routing templates
  * Host-side routing policies of Appendix B ("Policy Construction and Sharing", "Coverage
  * Accounting" and the layouts One, Zero, Band, Global, Row-Random, Aligned Sparse, BigBird,

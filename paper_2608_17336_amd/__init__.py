@@ -35,6 +35,9 @@ __all__ = [
     "tilemix_fit_template",
     "tilemix_varlen_workspace_size",
     "tilemix_prefill_varlen",
+    "tilemix_quantize_kv",
+    "tilemix_decode_workspace_size",
+    "tilemix_decode",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -53,6 +56,9 @@ EXPORTED_SYMBOLS = (
     "tilemix_fit_template",
     "tilemix_varlen_workspace_size",
     "tilemix_prefill_varlen",
+    "tilemix_quantize_kv",
+    "tilemix_decode_workspace_size",
+    "tilemix_decode",
     "tilemix_status_string",
     "tilemix_last_error",
 )
@@ -203,6 +209,12 @@ def load_library() -> ctypes.CDLL:
     lib.tilemix_prefill_varlen.argtypes = [P, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp, vp, vp,
                                            vp, vp, ctypes.c_size_t, vp]
     lib.tilemix_prefill_varlen.restype = ctypes.c_int
+    lib.tilemix_quantize_kv.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
+    lib.tilemix_quantize_kv.restype = ctypes.c_int
+    lib.tilemix_decode_workspace_size.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+    lib.tilemix_decode_workspace_size.restype = ctypes.c_int
+    lib.tilemix_decode.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.tilemix_decode.restype = ctypes.c_int
     lib.tilemix_route_coverage.argtypes = [P, vp, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_double)]
     lib.tilemix_route_coverage.restype = ctypes.c_int
@@ -476,4 +488,63 @@ def tilemix_prefill_varlen(Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q: int, 
     _check(load_library().tilemix_prefill_varlen(
         ctypes.byref(cp), total_q, total_k, _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), _ptr(Q), _ptr(K),
         _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace), ctypes.c_size_t(nbytes), _stream(stream)))
+    return O
+
+
+# ------------------------------------------------------------ INT8 key/value cache decode
+
+def tilemix_quantize_kv(K, V, *, stream=None):
+    """INT8 key/value cache of K, V [B, L_k, H_k, d] (fp16 CUDA): (K8, dK, V8, dV)."""
+    import torch
+    B, Lk, Hk, d = K.shape
+    p = Params(B, Hk, Hk, 1, Lk, d)
+    _require(K, torch.float16, (B, Lk, Hk, d), "K")
+    _require(V, torch.float16, (B, Lk, Hk, d), "V")
+    K8 = torch.empty((B, Lk, Hk, d), dtype=torch.int8, device=K.device)
+    V8 = torch.empty_like(K8)
+    dK = torch.empty((B, -(-Lk // 64), Hk), dtype=torch.float16, device=K.device)
+    dV = torch.empty_like(dK)
+    cp = p.c()
+    _check(load_library().tilemix_quantize_kv(ctypes.byref(cp), _ptr(K), _ptr(V), _ptr(K8), _ptr(dK),
+                                              _ptr(V8), _ptr(dV), _stream(stream)))
+    return K8, dK, V8, dV
+
+
+def tilemix_decode_workspace_size(params: Params) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().tilemix_decode_workspace_size(ctypes.byref(params.c()), ctypes.byref(n)))
+    return int(n.value)
+
+
+def tilemix_decode(Q, K, K8, dK, V8, dV, route_bits, group_size: int, scale: float | None = None,
+                   *, O=None, workspace=None, stream=None, route_per_batch: bool = False,
+                   route_hint: int = -1):
+    """One decode step: Q [B, 1, Hq, d] against the FP16 key cache K and the INT8 caches
+    (K8, dK, V8, dV) [B, L_k, H_k, d]; route_bits int64 CUDA [B_r, H_k, 1, W].  Returns O."""
+    import torch
+    B, Lq, Hq, d = Q.shape
+    Lk, Hk = K.shape[1], K.shape[2]
+    p = Params(B, Hq, Hk, Lq, Lk, d, 128, 64, group_size, True,
+               scale if scale else 1.0 / math.sqrt(d), route_per_batch, route_hint)
+    _require(Q, torch.float16, (B, 1, Hq, d), "Q")
+    _require(K, torch.float16, (B, Lk, Hk, d), "K")
+    _require(K8, torch.int8, (B, Lk, Hk, d), "K8")
+    _require(V8, torch.int8, (B, Lk, Hk, d), "V8")
+    _require(dK, torch.float16, (B, -(-Lk // 64), Hk), "dK")
+    _require(dV, torch.float16, (B, -(-Lk // 64), Hk), "dV")
+    _require(route_bits, torch.int64, (B if route_per_batch else 1, Hk, 1, tilemix_route_words_per_row(p)),
+             "route_bits")
+    if O is None:
+        O = torch.empty_like(Q)
+    _require(O, torch.float16, (B, 1, Hq, d), "O")
+    need = tilemix_decode_workspace_size(p)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=Q.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    if nbytes < need:
+        raise ValueError(f"workspace too small: {need} bytes needed")
+    cp = p.c()
+    _check(load_library().tilemix_decode(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(K8), _ptr(dK), _ptr(V8),
+                                         _ptr(dV), _ptr(route_bits), _ptr(O), _ptr(workspace),
+                                         ctypes.c_size_t(nbytes), _stream(stream)))
     return O

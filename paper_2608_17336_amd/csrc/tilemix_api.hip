@@ -317,6 +317,96 @@ tilemix_status tilemix_prefill_varlen(const tilemix_params* params, int32_t tota
   return ok();
 }
 
+namespace {
+
+tilemix_status check_decode(const tilemix_params* p) {
+  tilemix_status st = validate(p);
+  if (st != TILEMIX_OK) return st;
+  if (p->len_q != 1) return fail(TILEMIX_ERR_UNSUPPORTED, "decode takes one query token (len_q = 1)");
+  if (p->heads_q / p->heads_kv > tilemix::kDecMaxGroup)
+    return fail(TILEMIX_ERR_UNSUPPORTED, "decode supports at most %d query heads per KV head",
+                tilemix::kDecMaxGroup);
+  return TILEMIX_OK;
+}
+
+size_t decode_workspace(const tilemix_params* p) {
+  const size_t rows = (size_t)p->batch * p->heads_q * tilemix::decode_chunks(p->len_k);
+  return align256(rows * sizeof(float)) * 2 + align256(rows * p->head_dim * sizeof(float));
+}
+
+}  // namespace
+
+tilemix_status tilemix_quantize_kv(const tilemix_params* params, const void* K, const void* V,
+                                   int8_t* K8, uint16_t* dK, int8_t* V8, uint16_t* dV,
+                                   void* stream) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  const tilemix_params& p = *params;
+  if (!K || !V || !K8 || !dK || !V8 || !dV) return fail(TILEMIX_ERR_NULL, "NULL tensor pointer");
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(K8, 16) || !aligned(V8, 16) ||
+      !aligned(dK, 2) || !aligned(dV, 2))
+    return fail(TILEMIX_ERR_ALIGN, "K, V, K8, V8 must be 16-byte and dK, dV 2-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(K), K8, dK, p.batch, p.len_k,
+                                           p.heads_kv, p.head_dim, tilemix::kQuantBlockK, nullptr,
+                                           true, s), "quantize K");
+  if (st != TILEMIX_OK) return st;
+  st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(V), V8, dV, p.batch, p.len_k,
+                                           p.heads_kv, p.head_dim, tilemix::kQuantBlockK, nullptr,
+                                           true, s), "quantize V");
+  if (st != TILEMIX_OK) return st;
+  return ok();
+}
+
+tilemix_status tilemix_decode_workspace_size(const tilemix_params* params, size_t* bytes) {
+  tilemix_status st = check_decode(params);
+  if (st != TILEMIX_OK) return st;
+  if (!bytes) return fail(TILEMIX_ERR_NULL, "bytes is NULL");
+  *bytes = decode_workspace(params);
+  return ok();
+}
+
+tilemix_status tilemix_decode(const tilemix_params* params, const void* Q, const void* K,
+                              const int8_t* K8, const uint16_t* dK, const int8_t* V8,
+                              const uint16_t* dV, const uint64_t* route_bits, void* O,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  tilemix_status st = check_decode(params);
+  if (st != TILEMIX_OK) return st;
+  const tilemix_params& p = *params;
+  if (!Q || !K || !K8 || !dK || !V8 || !dV || !route_bits || !O)
+    return fail(TILEMIX_ERR_NULL, "NULL tensor pointer");
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(K8, 16) || !aligned(V8, 16) ||
+      !aligned(dK, 2) || !aligned(dV, 2) || !aligned(route_bits, 8) || !aligned(O, 16))
+    return fail(TILEMIX_ERR_ALIGN, "Q, K, K8, V8, O must be 16-byte, dK, dV 2-byte and "
+                "route_bits 8-byte aligned");
+  const size_t need = decode_workspace(params);
+  if (!workspace) return fail(TILEMIX_ERR_WORKSPACE, "workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(TILEMIX_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(TILEMIX_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  const Plan pl = make_plan(params);
+  tilemix::DecodeArgs a{};
+  a.Q = static_cast<const _Float16*>(Q);
+  a.K = static_cast<const _Float16*>(K);
+  a.K8 = K8; a.dK = dK; a.V8 = V8; a.dV = dV;
+  a.route = route_bits;
+  a.O = static_cast<_Float16*>(O);
+  a.B = p.batch; a.Hq = p.heads_q; a.Hk = p.heads_kv; a.Lk = p.len_k;
+  a.W = (int)pl.W; a.g = p.group_size; a.nKB = (int)pl.nKB;
+  a.chunks = tilemix::decode_chunks(p.len_k);
+  a.route_per_batch = p.route_per_batch;
+  a.force_fp16 = p.route_hint == 0 ? 1 : 0;
+  a.scale_log2e = p.scale * 1.4426950408889634f;
+  const size_t rows = (size_t)p.batch * p.heads_q * a.chunks;
+  char* ws = static_cast<char*>(workspace);
+  a.part_m = reinterpret_cast<float*>(ws);
+  a.part_z = reinterpret_cast<float*>(ws + align256(rows * sizeof(float)));
+  a.part_o = reinterpret_cast<float*>(ws + 2 * align256(rows * sizeof(float)));
+  st = hip_status(tilemix::launch_decode(a, p.head_dim, static_cast<hipStream_t>(stream)), "decode");
+  if (st != TILEMIX_OK) return st;
+  return ok();
+}
+
 tilemix_status tilemix_quantize(const tilemix_params* params, const void* Q, const void* K,
                                 int8_t* Q8, uint16_t* dQ, int8_t* K8, uint16_t* dK, void* stream) {
   tilemix_status st = validate(params);

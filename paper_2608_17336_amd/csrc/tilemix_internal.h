@@ -51,6 +51,25 @@ struct AttnArgs {
   float scale_log2e;      // softmax scale * log2(e)
 };
 
+// Arguments of the INT8 key/value cache decode kernels (one query token per sequence).
+constexpr int kDecMaxGroup = 16;   // query heads per KV head
+struct DecodeArgs {
+  const _Float16* Q;       // [B, Hq, d]
+  const _Float16* K;       // FP16 key cache [B, Lk, Hk, d] (FP16-routed groups)
+  const int8_t* K8;        // [B, Lk, Hk, d]
+  const uint16_t* dK;      // FP16 bits [B, nKB, Hk]
+  const int8_t* V8;        // [B, Lk, Hk, d]
+  const uint16_t* dV;      // FP16 bits [B, nKB, Hk]
+  const uint64_t* route;   // [B_r, Hk, 1, W]
+  _Float16* O;             // [B, Hq, d]
+  float* part_m;           // [B, Hq, chunks]: chunk max (log2 units)
+  float* part_z;           // [B, Hq, chunks]: chunk normalizer
+  float* part_o;           // [B, Hq, chunks, d]: chunk output, unnormalized
+  int B, Hq, Hk, Lk, W, g, nKB, chunks;
+  int route_per_batch, force_fp16;
+  float scale_log2e;
+};
+
 // Arguments of the INT32 tile-product check kernel.
 struct DebugTileArgs {
   const int8_t* Q8;
@@ -69,6 +88,8 @@ hipError_t launch_v_tiles(const _Float16* V, _Float16* Vt, int B, int L, int H, 
 hipError_t launch_seq_table(const int* cu_q, const int* cu_k, int batch, int total_q, int total_k,
                             int max_q, int max_k, int block_m, int* seqs, hipStream_t stream);
 hipError_t launch_routed_attention(const AttnArgs& args, int d, int block_m, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& args, int d, hipStream_t stream);
+int decode_chunks(int len_k);
 hipError_t launch_debug_tiles(const DebugTileArgs& args, int d, int block_m, hipStream_t stream);
 
 }  // namespace tilemix

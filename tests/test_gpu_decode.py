@@ -1,0 +1,63 @@
+"""GPU parity of the INT8 key/value cache decode path against the decode oracle."""
+
+import numpy as np
+import pytest
+
+from gpu_util import MAX_ABS, REL_L2, log, to_dev
+from oracle.decode import kv_cache, routed_decode
+from synth import make_qkv, pack_route_bits, small_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def test_quantize_kv_bitexact():
+    import paper_2608_17336_amd as tm
+    cfg = small_workload("kvq", B=2, Hq=2, Hk=2, d=128, L=333, k_outliers=True, index=910)
+    _, K, V = make_qkv(cfg)
+    V[1, 64:128, 0, :] = 0.0   # a zero block
+    k8, dk, v8, dv = [t.cpu().numpy() for t in tm.tilemix_quantize_kv(to_dev(K), to_dev(V))]
+    ok8, odk, ov8, odv = kv_cache(K, V)
+    np.testing.assert_array_equal(k8, ok8)
+    np.testing.assert_array_equal(v8, ov8)
+    np.testing.assert_array_equal(dk.view(np.uint16), odk.view(np.uint16))
+    np.testing.assert_array_equal(dv.view(np.uint16), odv.view(np.uint16))
+
+
+CASES = [
+    # B, Hq, Hk, d, L_k, g, route_per_batch
+    (2, 8, 2, 128, 5000, 4, False),
+    (1, 4, 4, 128, 1, 1, False),
+    (2, 4, 2, 128, 63, 1, True),
+    (1, 16, 1, 128, 700, 2, False),
+    (3, 6, 2, 64, 300, 1, False),
+    (1, 2, 1, 64, 257, 3, True),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hk,d,Lk,g,rpb", CASES, ids=[str(c) for c in CASES])
+def test_decode_parity(B, Hq, Hk, d, Lk, g, rpb):
+    import torch
+    import paper_2608_17336_amd as tm
+    cfg = small_workload("dec", B=B, Hq=Hq, Hk=Hk, d=d, L=Lk, group_size=g, k_outliers=True,
+                         index=920 + Lk)
+    Q, K, V = make_qkv(cfg)
+    Q1 = np.ascontiguousarray(Q[:, -1:])
+    k, v = to_dev(K), to_dev(V)
+    K8, dK, V8, dV = tm.tilemix_quantize_kv(k, v)
+    ck = [t.cpu().numpy() for t in (K8, dK, V8, dV)]
+    T_mask = -(-(-(-Lk // 64)) // g)
+    rng = np.random.default_rng(Lk)
+    for p in (0.5, 0.0, 1.0):
+        R = (rng.random((B if rpb else 1, Hk, 1, T_mask)) < p).astype(np.uint8)
+        words = np.concatenate([pack_route_bits(R[i]) for i in range(R.shape[0])], axis=0)
+        log(f"decode B={B} Hq={Hq} Hk={Hk} d={d} Lk={Lk} g={g} rpb={rpb} p={p}")
+        O = tm.tilemix_decode(to_dev(Q1), k, K8, dK, V8, dV, to_dev(words), g, cfg.scale,
+                              route_per_batch=rpb, route_hint=0 if p == 0.0 else -1)
+        torch.cuda.synchronize()
+        got = O.float().cpu().numpy().astype(np.float64)
+        ref = routed_decode(Q1, K, *ck, words, g, cfg.scale)
+        diff = got - ref
+        mx = float(np.abs(diff).max())
+        rel = float(np.sqrt((diff ** 2).sum() / (ref ** 2).sum()))
+        log(f"  max_abs={mx:.3e} rel_l2={rel:.3e}")
+        assert mx <= MAX_ABS and rel <= REL_L2, (p, mx, rel)
