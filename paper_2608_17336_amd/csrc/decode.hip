@@ -30,6 +30,7 @@ constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
 constexpr int kDecChunk = 512;                  // keys per workgroup
 constexpr int kKeysPerThread = kDecChunk / kDecThreads;
+constexpr int kDecMaxChunks = (kMaxKeyTiles * kBlockN) / kDecChunk;   // chunks of the longest cache
 
 __device__ __forceinline__ float wave_max(float v) {
   for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
@@ -243,24 +244,54 @@ __global__ __launch_bounds__(kDecThreads) void decode_partial_kernel(DecodeArgs 
   }
 }
 
+// One workgroup per (sequence, query head): the chunks' maxima give m; each chunk's weight
+// 2^(m_i - m) goes to LDS with the normalizer z = sum z_i 2^(m_i - m); then threads over
+// (channel, chunk residue) add the weighted chunk outputs and the residues are summed in LDS.
 template <int D>
-__global__ __launch_bounds__(D) void decode_combine_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(DecodeArgs a) {
+  constexpr int kParts = kDecThreads / D;
   const int bh = blockIdx.x;   // b * Hq + hq
-  const int c = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  __shared__ float wgt[kDecMaxChunks];
+  __shared__ float red[kDecWaves];
+  __shared__ float opart[kParts][D];
   const float* pm = a.part_m + (size_t)bh * a.chunks;
   const float* pz = a.part_z + (size_t)bh * a.chunks;
   float m = -__builtin_huge_valf();
-  for (int i = 0; i < a.chunks; ++i) m = fmaxf(m, pm[i]);
-  float z = 0.0f, o = 0.0f;
-  if (m != -__builtin_huge_valf()) {
-    for (int i = 0; i < a.chunks; ++i) {
-      if (pm[i] == -__builtin_huge_valf()) continue;
-      const float f = __builtin_amdgcn_exp2f(pm[i] - m);
-      z += pz[i] * f;
-      o += a.part_o[((size_t)bh * a.chunks + i) * D + c] * f;
-    }
+  for (int i = tid; i < a.chunks; i += kDecThreads) m = fmaxf(m, pm[i]);
+  m = wave_max(m);
+  if (lane == 0) red[wave] = m;
+  __syncthreads();
+  m = red[0];
+#pragma unroll
+  for (int w = 1; w < kDecWaves; ++w) m = fmaxf(m, red[w]);
+  float zl = 0.0f;
+  for (int i = tid; i < a.chunks; i += kDecThreads) {
+    const float f = (m == -__builtin_huge_valf() || pm[i] == -__builtin_huge_valf())
+                        ? 0.0f : __builtin_amdgcn_exp2f(pm[i] - m);
+    wgt[i] = f;
+    zl += pz[i] * f;
   }
-  a.O[(size_t)bh * D + c] = (_Float16)(z > 0.0f ? o / z : 0.0f);
+  zl = wave_sum(zl);
+  __syncthreads();   // red is reused
+  if (lane == 0) red[wave] = zl;
+  __syncthreads();
+  float z = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kDecWaves; ++w) z += red[w];
+  const int c = tid % D, part = tid / D;
+  const float* po = a.part_o + (size_t)bh * a.chunks * D + c;
+  float o = 0.0f;
+#pragma unroll 4
+  for (int i = part; i < a.chunks; i += kParts) o += po[(size_t)i * D] * wgt[i];
+  opart[part][c] = o;
+  __syncthreads();
+  if (tid < D) {
+    float t = 0.0f;
+#pragma unroll
+    for (int r = 0; r < kParts; ++r) t += opart[r][tid];
+    a.O[(size_t)bh * D + tid] = (_Float16)(z > 0.0f ? t / z : 0.0f);
+  }
 }
 
 template <int D, int GP>
@@ -278,7 +309,7 @@ hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t stream) {
   else if (G <= 8) launch_partial<D, 8>(a, stream);
   else if (G <= 16) launch_partial<D, 16>(a, stream);
   else return hipErrorInvalidValue;
-  hipLaunchKernelGGL(decode_combine_kernel<D>, dim3(a.B * a.Hq), dim3(D), 0, stream, a);
+  hipLaunchKernelGGL(decode_combine_kernel<D>, dim3(a.B * a.Hq), dim3(kDecThreads), 0, stream, a);
   return hipGetLastError();
 }
 
