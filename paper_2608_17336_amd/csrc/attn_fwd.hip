@@ -490,9 +490,11 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     ++iss_vt;
     iss_v += (size_t)D * kBlockN * 2;
   };
+  // Every sync below frees exactly one K and one V slot, so at most one tile of each kind is
+  // pending at a call.
   auto issue = [&](int k_last, int v_last) {
-    for (const int l = min(k_last, n_end); iss_kt <= l;) issue_k_next();
-    for (const int l = min(v_last, n_end); iss_vt <= l;) issue_v_next();
+    if (iss_kt <= min(k_last, n_end)) issue_k_next();
+    if (iss_vt <= min(v_last, n_end)) issue_v_next();
   };
   auto route_of = [&](int n) -> bool { return (route_ring >> (n & 63)) & 1ull; };   // issued K n
   // Every copy issued so far has landed for every wave, then K through k_last and V through
@@ -689,7 +691,8 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   const int wg_first_row_last_key = min(Lk - 1, m * BM + off);
   const int n_split = max(0, min(n_end + 1, (wg_first_row_last_key + 1) / kBlockN));
 
-  issue(1, 0);   // K of tiles 0 and 1, V of tile 0
+  issue(0, 0);   // K and V of tile 0, then K of tile 1
+  issue(1, 0);
   wait_all_memory();
   __syncthreads();
 
