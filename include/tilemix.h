@@ -190,9 +190,13 @@ tilemix_status tilemix_prefill_varlen(const tilemix_params* params, int32_t tota
  * applied to K and to V).  During decode, cached K8 takes the INT8 score path; cached V8 is
  * widened on chip with its block scale folded into the probabilities before P.V.
  *
- * tilemix_quantize_kv -- build the cache: K8/V8 int8 [B, L_k, H_k, d] and dK/dV FP16 bits
- * [B, ceil(L_k/64), H_k] from device FP16 K, V [B, L_k, H_k, d] (same rules as
- * tilemix_quantize).  K8, V8 16-byte and dK, dV 2-byte aligned.
+ * tilemix_quantize_kv -- build the cache from device FP16 K, V [B, L_k, H_k, d] (same rules as
+ * tilemix_quantize):
+ *   K8      int8 [B, L_k, H_k, d] (key rows, the layout of K)
+ *   V8      int8 [B, H_k, ceil(L_k/64), d, 64]: each 64-key block stored channel-major (V^T),
+ *           keys past L_k in the last block 0
+ *   dK, dV  FP16 bits [B, ceil(L_k/64), H_k]
+ * K8, V8 16-byte and dK, dV 2-byte aligned.
  */
 tilemix_status tilemix_quantize_kv(const tilemix_params* params, const void* K, const void* V,
                                    int8_t* K8, uint16_t* dK, int8_t* V8, uint16_t* dV,
@@ -210,7 +214,7 @@ tilemix_status tilemix_decode_workspace_size(const tilemix_params* params, size_
  *   Q, O        device FP16 [B, 1, H_q, d]
  *   K           device FP16 key cache [B, L_k, H_k, d], read for FP16-routed groups
  *   K8, dK      device INT8 key cache and scales (tilemix_quantize_kv), INT8-routed groups
- *   V8, dV      device INT8 value cache and scales
+ *   V8, dV      device INT8 value cache (the transposed-block layout above) and scales
  *   route_bits  device uint64 [B_r, H_k, 1, W]
  *   workspace   >= tilemix_decode_workspace_size() bytes, 256-byte aligned
  * Scores follow tilemix_prefill (the query's INT8 codes use its own row as the block); the

@@ -494,14 +494,15 @@ def tilemix_prefill_varlen(Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q: int, 
 # ------------------------------------------------------------ INT8 key/value cache decode
 
 def tilemix_quantize_kv(K, V, *, stream=None):
-    """INT8 key/value cache of K, V [B, L_k, H_k, d] (fp16 CUDA): (K8, dK, V8, dV)."""
+    """INT8 key/value cache of K, V [B, L_k, H_k, d] (fp16 CUDA): (K8, dK, V8, dV) with K8
+    [B, L_k, H_k, d] and V8 [B, H_k, ceil(L_k/64), d, 64] (each 64-key block channel-major)."""
     import torch
     B, Lk, Hk, d = K.shape
     p = Params(B, Hk, Hk, 1, Lk, d)
     _require(K, torch.float16, (B, Lk, Hk, d), "K")
     _require(V, torch.float16, (B, Lk, Hk, d), "V")
     K8 = torch.empty((B, Lk, Hk, d), dtype=torch.int8, device=K.device)
-    V8 = torch.empty_like(K8)
+    V8 = torch.empty((B, Hk, -(-Lk // 64), d, 64), dtype=torch.int8, device=K.device)
     dK = torch.empty((B, -(-Lk // 64), Hk), dtype=torch.float16, device=K.device)
     dV = torch.empty_like(dK)
     cp = p.c()
@@ -519,8 +520,8 @@ def tilemix_decode_workspace_size(params: Params) -> int:
 def tilemix_decode(Q, K, K8, dK, V8, dV, route_bits, group_size: int, scale: float | None = None,
                    *, O=None, workspace=None, stream=None, route_per_batch: bool = False,
                    route_hint: int = -1):
-    """One decode step: Q [B, 1, Hq, d] against the FP16 key cache K and the INT8 caches
-    (K8, dK, V8, dV) [B, L_k, H_k, d]; route_bits int64 CUDA [B_r, H_k, 1, W].  Returns O."""
+    """One decode step: Q [B, 1, Hq, d] against the FP16 key cache K [B, L_k, H_k, d] and the
+    INT8 caches of tilemix_quantize_kv; route_bits int64 CUDA [B_r, H_k, 1, W].  Returns O."""
     import torch
     B, Lq, Hq, d = Q.shape
     Lk, Hk = K.shape[1], K.shape[2]
@@ -529,7 +530,7 @@ def tilemix_decode(Q, K, K8, dK, V8, dV, route_bits, group_size: int, scale: flo
     _require(Q, torch.float16, (B, 1, Hq, d), "Q")
     _require(K, torch.float16, (B, Lk, Hk, d), "K")
     _require(K8, torch.int8, (B, Lk, Hk, d), "K8")
-    _require(V8, torch.int8, (B, Lk, Hk, d), "V8")
+    _require(V8, torch.int8, (B, Hk, -(-Lk // 64), d, 64), "V8")
     _require(dK, torch.float16, (B, -(-Lk // 64), Hk), "dK")
     _require(dV, torch.float16, (B, -(-Lk // 64), Hk), "dV")
     _require(route_bits, torch.int64, (B if route_per_batch else 1, Hk, 1, tilemix_route_words_per_row(p)),

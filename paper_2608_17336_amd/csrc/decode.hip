@@ -9,14 +9,16 @@
 // by HBM bandwidth; a split-K layout spreads each (sequence, KV head) stream over many
 // workgroups.
 //
-//   decode_partial_kernel<D, GP>: workgroup (chunk of 512 keys, KV head, sequence), GP >= G
-//     query heads of the GQA group (the padding heads carry no weight).  The group's query
-//     rows are quantized on chip (the lone decode row is a whole 128-row quantization block);
-//     each thread scores two keys on their routed path for every head; one max and one sum
-//     reduction per chunk give the chunk's max and normalizer; then each wave accumulates
-//     P * dV against V8 over its quarter of the chunk, lanes over 4-channel slots, and the
-//     waves' partial outputs are added through LDS.  Writes (max, normalizer, unnormalized
-//     output) per (sequence, query head, chunk).
+//   decode_partial_kernel<D>: workgroup (chunk of 512 keys, KV head, sequence), the G <= 16
+//     query heads of the GQA group on the rows of 16x16 matrix-core tiles (padding rows carry
+//     no weight).  The group's query rows are quantized on chip (the lone decode row is a
+//     whole 128-row quantization block).  Each wave scores its 128 keys in 16-key blocks on
+//     the block's routed path (v_mfma_i32_16x16x64_i8 on K8 rows, v_mfma_f32_16x16x32_f16 on
+//     FP16 key rows); one max and one sum reduction give the chunk's max and normalizer per
+//     head; P * dV goes to LDS in FP16 and the wave accumulates O^T += V^T (P dV)^T with
+//     v_mfma_f32_16x16x32_f16, V^T read from the transposed value-cache tiles and widened to
+//     FP16 exactly.  The waves' partial outputs are added through LDS.  Writes (max,
+//     normalizer, unnormalized output) per (sequence, query head, chunk).
 //   decode_combine_kernel: merges the chunks of one (sequence, query head) with the
 //     log-sum-exp rule and writes O in FP16.
 #include "tilemix_device.h"
@@ -29,7 +31,7 @@ namespace {
 constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
 constexpr int kDecChunk = 512;                  // keys per workgroup
-constexpr int kKeysPerThread = kDecChunk / kDecThreads;
+constexpr int kDecHeads = 16;                   // query heads per KV head the MFMA rows hold
 constexpr int kDecMaxChunks = (kMaxKeyTiles * kBlockN) / kDecChunk;   // chunks of the longest cache
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -41,22 +43,49 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-template <int D, int GP>
+// Eight int8 codes (one per byte of v) widened to FP16, exactly: with the sign bit flipped a
+// byte b reads as 1024 + 128 + b in the FP16 pattern 0x64xx, and 1152 is then subtracted.
+__device__ __forceinline__ half8 i8x8_to_half8(uint2 v) {
+  const uint32_t lo = v.x ^ 0x80808080u, hi = v.y ^ 0x80808080u;
+  const half2v bias = {(_Float16)-1152.0f, (_Float16)-1152.0f};
+  half8 out;
+  const uint32_t w[2] = {lo, hi};
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    // bytes 0,1 -> halves 0x64b0, 0x64b1; bytes 2,3 -> 0x64b2, 0x64b3
+    const uint32_t p01 = __builtin_amdgcn_perm(0x64646464u, w[i], 0x07010700u);
+    const uint32_t p23 = __builtin_amdgcn_perm(0x64646464u, w[i], 0x07030702u);
+    const half2v h01 = __builtin_bit_cast(half2v, p01) + bias;
+    const half2v h23 = __builtin_bit_cast(half2v, p23) + bias;
+    out[4 * i + 0] = h01[0]; out[4 * i + 1] = h01[1];
+    out[4 * i + 2] = h23[0]; out[4 * i + 3] = h23[1];
+  }
+  return out;
+}
+
+template <int D>
 __global__ __launch_bounds__(kDecThreads) void decode_partial_kernel(DecodeArgs a) {
-  constexpr int kRowDwords = D / 4;               // dwords of one V8 row
-  constexpr int kKeysPerIter = kWave / kRowDwords; // keys one wave reads per load
+  constexpr int kKeysPerWave = kDecChunk / kDecWaves;   // 128
+  constexpr int kBlocks = kKeysPerWave / 16;             // 16-key score blocks per wave
+  constexpr int kSteps = kKeysPerWave / 32;              // 32-key P.V steps per wave
+  constexpr int kCB = D / 16;                            // 16-channel output blocks
   const int chunk = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
   const int G = a.Hq / a.Hk;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
-  __shared__ __align__(16) _Float16 q16[GP][D];
-  __shared__ __align__(16) int8_t q8[GP][D];
-  __shared__ float cq[GP];                                   // scale * log2(e) * dQ per head
-  __shared__ __align__(16) float pv[GP * kDecChunk];         // scores, P * dV; then outputs
-  __shared__ float red[2][GP][kDecWaves];
+  const int l16 = lane & 15, lq = lane >> 4;
+  __shared__ __align__(16) _Float16 q16[kDecHeads][D];
+  __shared__ __align__(16) int8_t q8[kDecHeads][D];
+  __shared__ float cq[kDecHeads];                         // scale * log2(e) * dQ per head
+  // P * dV [head][key] in FP16 for the P.V step, then the waves' partial outputs [wave][head][D]
+  constexpr int kPhBytes = kDecHeads * kDecChunk * 2, kOsumBytes = kDecWaves * kDecHeads * D * 4;
+  __shared__ __align__(16) char buf[kPhBytes > kOsumBytes ? kPhBytes : kOsumBytes];
+  auto ph = reinterpret_cast<_Float16(*)[kDecChunk]>(buf);
+  auto osum = reinterpret_cast<float(*)[kDecHeads][D]>(buf);
+  __shared__ float red[2][kDecWaves][kDecHeads];
 
   // 1. Query rows of the group: FP16 copy, INT8 codes and FP16-stored scale (Appendix C
-  //    quantization; the lone decode row forms its own 128-row block).  Padding heads are 0.
-  for (int g = wave; g < GP; g += kDecWaves) {
+  //    quantization; the lone decode row forms its own 128-row block).  Rows past G are 0.
+  for (int g = wave; g < kDecHeads; g += kDecWaves) {
     const int hq = hk * G + g;
     float x[D / 64];
     float amax = 0.0f;
@@ -78,168 +107,151 @@ __global__ __launch_bounds__(kDecThreads) void decode_partial_kernel(DecodeArgs 
   }
   __syncthreads();
 
-  // 2. Scores of this thread's keys for every head, log2 domain; lane max per head.
-  float lmax[GP];
+  // 2. Scores S[head][key] of the wave's 128 keys, 16 keys per block, on the matrix cores:
+  //    v_mfma_i32_16x16x64_i8 (INT8 route) or v_mfma_f32_16x16x32_f16 (FP16 route), heads on
+  //    the rows (A from LDS) and keys on the columns (B straight from the key rows).  Lane l
+  //    holds heads 4*(l/16) + r of key l % 16.
+  i32x4 qa8[D / 64];
+  half8 qa16[D / 32];
 #pragma unroll
-  for (int g = 0; g < GP; ++g) lmax[g] = -__builtin_huge_valf();
+  for (int s = 0; s < D / 64; ++s) qa8[s] = *reinterpret_cast<const i32x4*>(&q8[l16][64 * s + 16 * lq]);
 #pragma unroll
-  for (int u = 0; u < kKeysPerThread; ++u) {
-    const int t = u * kDecThreads + tid;                     // key within the chunk
-    const int j = chunk * kDecChunk + t;
-    const bool valid = j < a.Lk;
-    // key tile of the wave's keys (clamped for the keys past L_k of the last chunk)
-    const int n = min(__builtin_amdgcn_readfirstlane(j >> 6), a.nKB - 1);
+  for (int s = 0; s < D / 32; ++s) qa16[s] = *reinterpret_cast<const half8*>(&q16[l16][32 * s + 8 * lq]);
+  float cqr[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) cqr[r] = cq[4 * lq + r];
+  const int key_base = chunk * kDecChunk + wave * kKeysPerWave;
+  float sc[kBlocks][4];
+#pragma unroll
+  for (int jb = 0; jb < kBlocks; ++jb) {
+    const int k0 = key_base + 16 * jb;
+    const int n = min(k0 >> 6, a.nKB - 1);   // key tile of the block (clamped past L_k)
     const int gj = n / a.g;
     const uint64_t word = a.route[((size_t)(a.route_per_batch ? b : 0) * a.Hk + hk) * a.W + (gj >> 6)];
     const bool int8 = !a.force_fp16 && ((word >> (gj & 63)) & 1ull);
-    const float dk = half_bits_to_float(a.dK[((size_t)b * a.nKB + n) * a.Hk + hk]);
-    const size_t row = ((size_t)b * a.Lk + (valid ? j : 0)) * a.Hk + hk;
-    float s[GP];
+    const int key = k0 + l16;
+    const bool valid = key < a.Lk;
+    const size_t row = ((size_t)b * a.Lk + (valid ? key : 0)) * a.Hk + hk;
+    float v[4];
     if (int8) {
-      int kw[D / 4];
+      const float dk = half_bits_to_float(a.dK[((size_t)b * a.nKB + n) * a.Hk + hk]);
+      i32x4 acc = {0, 0, 0, 0};
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const uint4 v = ld_global_16(a.K8 + row * D + 16 * c);
-        kw[4 * c] = (int)v.x; kw[4 * c + 1] = (int)v.y; kw[4 * c + 2] = (int)v.z; kw[4 * c + 3] = (int)v.w;
+      for (int s = 0; s < D / 64; ++s) {
+        const i32x4 kb = as_i32x4(ld_global_16(a.K8 + row * D + 64 * s + 16 * lq));
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(qa8[s], kb, acc, 0, 0, 0);
       }
 #pragma unroll
-      for (int g = 0; g < GP; ++g) {
-        const int* qw = reinterpret_cast<const int*>(q8[g]);
-        int acc = 0;
-#pragma unroll
-        for (int c = 0; c < D / 4; ++c) acc = __builtin_amdgcn_sdot4(kw[c], qw[c], acc, false);
-        s[g] = (float)acc * (cq[g] * dk);
-      }
+      for (int r = 0; r < 4; ++r) v[r] = (float)acc[r] * (cqr[r] * dk);
     } else {
-      half2v kh[D / 2];
+      f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int c = 0; c < D / 8; ++c) {
-        const half8 v = as_half8(ld_global_16(a.K + row * D + 8 * c));
-#pragma unroll
-        for (int e = 0; e < 4; ++e) kh[4 * c + e] = half2v{v[2 * e], v[2 * e + 1]};
+      for (int s = 0; s < D / 32; ++s) {
+        const half8 kb = as_half8(ld_global_16(a.K + row * D + 32 * s + 8 * lq));
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa16[s], kb, acc, 0, 0, 0);
       }
 #pragma unroll
-      for (int g = 0; g < GP; ++g) {
-        const half2v* qh = reinterpret_cast<const half2v*>(q16[g]);
-        float acc = 0.0f;
-#pragma unroll
-        for (int c = 0; c < D / 2; ++c) acc = __builtin_amdgcn_fdot2(kh[c], qh[c], acc, false);
-        s[g] = acc * a.scale_log2e;
-      }
+      for (int r = 0; r < 4; ++r) v[r] = acc[r] * a.scale_log2e;
     }
 #pragma unroll
-    for (int g = 0; g < GP; ++g) {
-      const float v = (valid && g < G) ? s[g] : -__builtin_huge_valf();
-      pv[g * kDecChunk + t] = v;
-      lmax[g] = fmaxf(lmax[g], v);
-    }
+    for (int r = 0; r < 4; ++r) sc[jb][r] = (valid && 4 * lq + r < G) ? v[r] : -__builtin_huge_valf();
   }
+
+  // 3. Per-head chunk max and normalizer (the 16 lanes of a quarter-wave share their heads);
+  //    P * dV to LDS in FP16 for the P.V step (the V block scale folded into P).
+  float mx[4];
 #pragma unroll
-  for (int g = 0; g < GP; ++g) {
-    const float m = wave_max(lmax[g]);
-    if (lane == 0) red[0][g][wave] = m;
+  for (int r = 0; r < 4; ++r) {
+    float m = sc[0][r];
+#pragma unroll
+    for (int jb = 1; jb < kBlocks; ++jb) m = fmaxf(m, sc[jb][r]);
+#pragma unroll
+    for (int x = 1; x < 16; x <<= 1) m = fmaxf(m, __shfl_xor(m, x, kWave));
+    mx[r] = m;
+  }
+  if (l16 == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[0][wave][4 * lq + r] = mx[r];
   }
   __syncthreads();
-
-  // 3. Chunk max and normalizer per head; P * dV for the P.V step.
-  float m[GP], lz[GP];
+  float zs[4];
 #pragma unroll
-  for (int g = 0; g < GP; ++g) {
-    m[g] = red[0][g][0];
+  for (int r = 0; r < 4; ++r) {
+    float m = red[0][0][4 * lq + r];
 #pragma unroll
-    for (int w = 1; w < kDecWaves; ++w) m[g] = fmaxf(m[g], red[0][g][w]);
-    lz[g] = 0.0f;
+    for (int w = 1; w < kDecWaves; ++w) m = fmaxf(m, red[0][w][4 * lq + r]);
+    mx[r] = m;
+    zs[r] = 0.0f;
   }
 #pragma unroll
-  for (int u = 0; u < kKeysPerThread; ++u) {
-    const int t = u * kDecThreads + tid;
+  for (int jb = 0; jb < kBlocks; ++jb) {
+    const int t = wave * kKeysPerWave + 16 * jb + l16;           // key within the chunk
     const int n = min((chunk * kDecChunk + t) >> 6, a.nKB - 1);
     const float dv = half_bits_to_float(a.dV[((size_t)b * a.nKB + n) * a.Hk + hk]);
 #pragma unroll
-    for (int g = 0; g < GP; ++g) {
-      const float sc = pv[g * kDecChunk + t];
-      const float p = (m[g] == -__builtin_huge_valf()) ? 0.0f : __builtin_amdgcn_exp2f(sc - m[g]);
-      lz[g] += p;
-      pv[g * kDecChunk + t] = p * dv;
+    for (int r = 0; r < 4; ++r) {
+      const float p = (mx[r] == -__builtin_huge_valf()) ? 0.0f : __builtin_amdgcn_exp2f(sc[jb][r] - mx[r]);
+      zs[r] += p;
+      ph[4 * lq + r][t] = (_Float16)(p * dv);
     }
   }
 #pragma unroll
-  for (int g = 0; g < GP; ++g) {
-    const float z = wave_sum(lz[g]);
-    if (lane == 0) red[1][g][wave] = z;
+  for (int r = 0; r < 4; ++r) {
+    float z = zs[r];
+#pragma unroll
+    for (int x = 1; x < 16; x <<= 1) z += __shfl_xor(z, x, kWave);
+    zs[r] = z;
+  }
+  if (l16 == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[1][wave][4 * lq + r] = zs[r];
   }
   __syncthreads();
   if (tid < G) {
-    float z = 0.0f;
+    float z = 0.0f, m = red[0][0][tid];
 #pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) z += red[1][tid][w];
+    for (int w = 0; w < kDecWaves; ++w) {
+      z += red[1][w][tid];
+      m = fmaxf(m, red[0][w][tid]);
+    }
     const size_t o = ((size_t)b * a.Hq + hk * G + tid) * a.chunks + chunk;
-    float mm = red[0][tid][0];
-#pragma unroll
-    for (int w = 1; w < kDecWaves; ++w) mm = fmaxf(mm, red[0][tid][w]);
-    a.part_m[o] = mm;
+    a.part_m[o] = m;
     a.part_z[o] = z;
   }
 
-  // 4. O_g[c] = sum over the chunk's keys of (P dV)_g,j * V8[j][c]: wave w takes keys
-  //    [w, w + kDecWaves, ...) in steps of kKeysPerIter, each lane one 4-channel slot of one key.
-  const int kmax = min(kDecChunk, a.Lk - chunk * kDecChunk);
-  const int c4 = lane % kRowDwords, ksub = lane / kRowDwords;
-  const int8_t* vchunk = a.V8 + (((size_t)b * a.Lk + (size_t)chunk * kDecChunk) * a.Hk + hk) * D + 4 * c4;
-  const size_t vstride = (size_t)a.Hk * D;   // bytes between consecutive keys
-  float acc[GP][4];
+  // 4. O^T[channel][head] += V^T[channel][key] (P dV)^T[key][head], v_mfma_f32_16x16x32_f16:
+  //    A = 8 consecutive keys of one channel from the transposed V8 tile (widened to FP16),
+  //    B = 8 keys of P dV for one head from LDS.  Lane l ends with channels 4*(l/16) + r of
+  //    its 16-channel block for head l % 16.
+  f32x4 acc[kCB];
 #pragma unroll
-  for (int g = 0; g < GP; ++g)
+  for (int cb = 0; cb < kCB; ++cb) acc[cb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) acc[g][e] = 0.0f;
-  // Loads are issued kBatch keys at a time ahead of their arithmetic, so that each wave keeps
-  // kBatch rows in flight; keys past L_k read as 0 and carry P = 0.
-  constexpr int kStep = kDecWaves * kKeysPerIter;
-  constexpr int kBatch = 16;
-  for (int t0 = wave * kKeysPerIter; t0 < kmax; t0 += kStep * kBatch) {
-    uint32_t w[kBatch];
+  for (int st = 0; st < kSteps; ++st) {
+    const int kk = wave * kKeysPerWave + 32 * st;                // first key of the step (chunk)
+    const int key0 = chunk * kDecChunk + kk;
+    if (key0 >= a.Lk) break;                                     // the rest of the chunk is past L_k
+    const int n = key0 >> 6;
+    const half8 pb = *reinterpret_cast<const half8*>(&ph[l16][kk + 8 * lq]);
+    const int8_t* vt = a.V8 + ((((size_t)b * a.Hk + hk) * a.nKB + n) * D + l16) * kBlockN +
+                       (key0 & 63) + 8 * lq;
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int t = t0 + u * kStep + ksub;
-      w[u] = t < kmax ? *reinterpret_cast<const uint32_t*>(vchunk + (size_t)t * vstride) : 0u;
-    }
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int t = min(t0 + u * kStep + ksub, kDecChunk - 1);
-      float v[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = (float)(int8_t)(uint8_t)(w[u] >> (8 * e));
-#pragma unroll
-      for (int g = 0; g < GP; ++g) {
-        const float p = pv[g * kDecChunk + t];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[g][e] += p * v[e];
-      }
+    for (int cb = 0; cb < kCB; ++cb) {
+      const uint2 raw = *reinterpret_cast<const uint2*>(vt + (size_t)cb * 16 * kBlockN);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(i8x8_to_half8(raw), pb, acc[cb], 0, 0, 0);
     }
   }
-  // Lanes holding the same slot for different keys are added by lane exchange, the waves'
-  // partial outputs through LDS (pv is free again: [kDecWaves][GP][D] fits in it).
+  __syncthreads();   // every wave is done reading P before the buffer holds outputs
 #pragma unroll
-  for (int x = kRowDwords; x < kWave; x <<= 1)
+  for (int cb = 0; cb < kCB; ++cb)
 #pragma unroll
-    for (int g = 0; g < GP; ++g)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[g][e] += __shfl_xor(acc[g][e], x, kWave);
-  static_assert(kDecWaves * GP * D <= GP * kDecChunk, "partial outputs fit in pv");
-  __syncthreads();   // every wave is done reading pv
-  float* osum = pv;
-  if (ksub == 0) {
-#pragma unroll
-    for (int g = 0; g < GP; ++g)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) osum[(wave * GP + g) * D + 4 * c4 + e] = acc[g][e];
-  }
+    for (int r = 0; r < 4; ++r) osum[wave][l16][16 * cb + 4 * lq + r] = acc[cb][r];
   __syncthreads();
   for (int o = tid; o < G * D; o += kDecThreads) {
     const int g = o / D, c = o % D;
     float sum = 0.0f;
 #pragma unroll
-    for (int r = 0; r < kDecWaves; ++r) sum += osum[(r * GP + g) * D + c];
+    for (int w = 0; w < kDecWaves; ++w) sum += osum[w][g][c];
     a.part_o[(((size_t)b * a.Hq + hk * G + g) * a.chunks + chunk) * D + c] = sum;
   }
 }
@@ -294,21 +306,11 @@ __global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(DecodeArgs 
   }
 }
 
-template <int D, int GP>
-void launch_partial(const DecodeArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_partial_kernel<D, GP>), dim3(a.chunks, a.Hk, a.B), dim3(kDecThreads),
-                     0, stream, a);
-}
-
 template <int D>
 hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t stream) {
-  const int G = a.Hq / a.Hk;
-  if (G <= 1) launch_partial<D, 1>(a, stream);
-  else if (G <= 2) launch_partial<D, 2>(a, stream);
-  else if (G <= 4) launch_partial<D, 4>(a, stream);
-  else if (G <= 8) launch_partial<D, 8>(a, stream);
-  else if (G <= 16) launch_partial<D, 16>(a, stream);
-  else return hipErrorInvalidValue;
+  if (a.Hq / a.Hk > kDecHeads) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((decode_partial_kernel<D>), dim3(a.chunks, a.Hk, a.B), dim3(kDecThreads), 0,
+                     stream, a);
   hipLaunchKernelGGL(decode_combine_kernel<D>, dim3(a.B * a.Hq), dim3(kDecThreads), 0, stream, a);
   return hipGetLastError();
 }

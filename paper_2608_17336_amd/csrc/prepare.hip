@@ -45,7 +45,9 @@ __device__ __forceinline__ SeqRows seq_rows(const int* seqs, int b, int L, int n
   return SeqRows{e[f_start], e[f_blk], e[f_len]};
 }
 
-template <int D, int BLK>
+// TRANSPOSED (64-row blocks only): the codes of block r of head h go out as one [D][64] tile,
+// [B, H, nblk, D, 64], rows past the sequence end as 0 (the INT8 value-cache layout of decode).
+template <int D, int BLK, bool TRANSPOSED = false>
 __global__ __launch_bounds__(kPrepThreads) void quantize_blocks_kernel(
     const _Float16* __restrict__ X, int8_t* __restrict__ X8, uint16_t* __restrict__ dX,
     int L, int H, int nblk, const int* __restrict__ seqs, int f_start, int f_len, int f_blk) {
@@ -95,8 +97,18 @@ __global__ __launch_bounds__(kPrepThreads) void quantize_blocks_kernel(
           packed[e >> 2] |= byte << (8 * (e & 3));
         }
       }
-      const size_t off = ((size_t)(sq.start + row0 + row) * H + h) * D + ch * 8;
-      *reinterpret_cast<uint2*>(X8 + off) = make_uint2(packed[0], packed[1]);
+      if constexpr (TRANSPOSED) {
+        int8_t* t = X8 + (((size_t)b * H + h) * nblk + r) * (size_t)(D * BLK) + (size_t)(ch * 8) * BLK + row;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t[e * BLK] = (int8_t)(packed[e >> 2] >> (8 * (e & 3)));
+      } else {
+        const size_t off = ((size_t)(sq.start + row0 + row) * H + h) * D + ch * 8;
+        *reinterpret_cast<uint2*>(X8 + off) = make_uint2(packed[0], packed[1]);
+      }
+    } else if constexpr (TRANSPOSED) {   // padding keys of the last tile
+      int8_t* t = X8 + (((size_t)b * H + h) * nblk + r) * (size_t)(D * BLK) + (size_t)(ch * 8) * BLK + row;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e * BLK] = 0;
     }
   }
   if (threadIdx.x == 0) {
@@ -197,11 +209,22 @@ hipError_t launch_seq_table(const int* cu_q, const int* cu_k, int batch, int tot
 }
 
 hipError_t launch_quantize(const _Float16* X, int8_t* X8, uint16_t* dX, int B, int L, int H,
-                           int d, int block_rows, const int* seqs, bool keys, hipStream_t stream) {
+                           int d, int block_rows, const int* seqs, bool keys, hipStream_t stream,
+                           bool transposed) {
   const int nblk = (L + block_rows - 1) / block_rows;
   dim3 grid(nblk, H, B), block(kPrepThreads);
   const int fs = keys ? kSeqKStart : kSeqQStart, fl = keys ? kSeqKLen : kSeqQLen;
   const int fb = keys ? kSeqKBlk : kSeqQBlk;
+  if (transposed) {   // value cache: 64-row blocks, fixed lengths
+    if (seqs || block_rows != 64) return hipErrorInvalidValue;
+    if (d == 128)
+      hipLaunchKernelGGL((quantize_blocks_kernel<128, 64, true>), grid, block, 0, stream, X, X8, dX, L, H, nblk, seqs, fs, fl, fb);
+    else if (d == 64)
+      hipLaunchKernelGGL((quantize_blocks_kernel<64, 64, true>), grid, block, 0, stream, X, X8, dX, L, H, nblk, seqs, fs, fl, fb);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (d == 128 && block_rows == 128)
     hipLaunchKernelGGL((quantize_blocks_kernel<128, 128>), grid, block, 0, stream, X, X8, dX, L, H, nblk, seqs, fs, fl, fb);
   else if (d == 128 && block_rows == 64)

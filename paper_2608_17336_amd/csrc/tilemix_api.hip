@@ -353,7 +353,7 @@ tilemix_status tilemix_quantize_kv(const tilemix_params* params, const void* K, 
   if (st != TILEMIX_OK) return st;
   st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(V), V8, dV, p.batch, p.len_k,
                                            p.heads_kv, p.head_dim, tilemix::kQuantBlockK, nullptr,
-                                           true, s), "quantize V");
+                                           true, s, /*transposed=*/true), "quantize V");
   if (st != TILEMIX_OK) return st;
   return ok();
 }

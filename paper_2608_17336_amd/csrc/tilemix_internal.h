@@ -58,7 +58,7 @@ struct DecodeArgs {
   const _Float16* K;       // FP16 key cache [B, Lk, Hk, d] (FP16-routed groups)
   const int8_t* K8;        // [B, Lk, Hk, d]
   const uint16_t* dK;      // FP16 bits [B, nKB, Hk]
-  const int8_t* V8;        // [B, Lk, Hk, d]
+  const int8_t* V8;        // [B, Hk, nKB, d, 64]: per 64-key block, channel-major
   const uint16_t* dV;      // FP16 bits [B, nKB, Hk]
   const uint64_t* route;   // [B_r, Hk, 1, W]
   _Float16* O;             // [B, Hq, d]
@@ -81,8 +81,10 @@ struct DebugTileArgs {
 };
 
 // seqs: sequence table or nullptr (every sequence of length L); keys selects its K fields.
+// transposed: write 64-row blocks as [B, H, blocks, d, 64] tiles (the INT8 value cache).
 hipError_t launch_quantize(const _Float16* X, int8_t* X8, uint16_t* dX, int B, int L, int H,
-                           int d, int block_rows, const int* seqs, bool keys, hipStream_t stream);
+                           int d, int block_rows, const int* seqs, bool keys, hipStream_t stream,
+                           bool transposed = false);
 hipError_t launch_v_tiles(const _Float16* V, _Float16* Vt, int B, int L, int H, int d,
                           const int* seqs, hipStream_t stream);
 hipError_t launch_seq_table(const int* cu_q, const int* cu_k, int batch, int total_q, int total_k,

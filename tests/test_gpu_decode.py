@@ -18,7 +18,13 @@ def test_quantize_kv_bitexact():
     k8, dk, v8, dv = [t.cpu().numpy() for t in tm.tilemix_quantize_kv(to_dev(K), to_dev(V))]
     ok8, odk, ov8, odv = kv_cache(K, V)
     np.testing.assert_array_equal(k8, ok8)
-    np.testing.assert_array_equal(v8, ov8)
+    # V8 is stored per 64-key block channel-major: [B, H_k, blocks, d, 64], padding keys 0
+    B, L, Hk, d = V.shape
+    nb = -(-L // 64)
+    pad = np.zeros((B, nb * 64, Hk, d), np.int8)
+    pad[:, :L] = ov8
+    want = pad.reshape(B, nb, 64, Hk, d).transpose(0, 3, 1, 4, 2)
+    np.testing.assert_array_equal(v8, want)
     np.testing.assert_array_equal(dk.view(np.uint16), odk.view(np.uint16))
     np.testing.assert_array_equal(dv.view(np.uint16), odv.view(np.uint16))
 
@@ -44,7 +50,7 @@ def test_decode_parity(B, Hq, Hk, d, Lk, g, rpb):
     Q1 = np.ascontiguousarray(Q[:, -1:])
     k, v = to_dev(K), to_dev(V)
     K8, dK, V8, dV = tm.tilemix_quantize_kv(k, v)
-    ck = [t.cpu().numpy() for t in (K8, dK, V8, dV)]
+    ck = kv_cache(K, V)   # the oracle's own cache (bit-identical: test_quantize_kv_bitexact)
     T_mask = -(-(-(-Lk // 64)) // g)
     rng = np.random.default_rng(Lk)
     for p in (0.5, 0.0, 1.0):
