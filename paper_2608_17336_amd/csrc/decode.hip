@@ -9,14 +9,15 @@
 // by HBM bandwidth; a split-K layout spreads each (sequence, KV head) stream over many
 // workgroups.
 //
-//   decode_partial_kernel<D>: workgroup (chunk of 512 keys, KV head, sequence), the G <= 16
-//     query heads of the GQA group on the rows of 16x16 matrix-core tiles (padding rows carry
-//     no weight).  The group's query rows are quantized on chip (the lone decode row is a
-//     whole 128-row quantization block).  Each wave scores its 128 keys in 16-key blocks on
-//     the block's routed path (v_mfma_i32_16x16x64_i8 on K8 rows, v_mfma_f32_16x16x32_f16 on
-//     FP16 key rows); one max and one sum reduction give the chunk's max and normalizer per
-//     head; P * dV goes to LDS in FP16 and the wave accumulates O^T += V^T (P dV)^T with
-//     v_mfma_f32_16x16x32_f16, V^T read from the transposed value-cache tiles and widened to
+//   decode_partial_kernel<D>: workgroup (chunk of 512 keys, KV head, sequence), one 64-key
+//     tile per wave, the G <= 16 query heads of the GQA group on the columns of 16x16
+//     matrix-core tiles (padding columns carry no weight).  The tile's key rows and value
+//     rows are loaded once into registers; the group's query rows are quantized on chip (the
+//     lone decode row is a whole 128-row quantization block).  The wave scores its tile on the
+//     tile's routed path (v_mfma_i32_16x16x64_i8 on K8 rows, v_mfma_f32_16x16x32_f16 on FP16
+//     key rows); one max and one sum reduction give the chunk's max and normalizer per head;
+//     P * dV stays in registers as the FP16 operand of O^T += V^T (P dV)^T on
+//     v_mfma_f32_16x16x32_f16, V^T read from the transposed value-cache tile and widened to
 //     FP16 exactly.  The waves' partial outputs are added through LDS.  Writes (max,
 //     normalizer, unnormalized output) per (sequence, query head, chunk).
 //   decode_combine_kernel: merges the chunks of one (sequence, query head) with the
@@ -28,28 +29,18 @@ namespace tilemix {
 
 namespace {
 
-constexpr int kDecThreads = 256;
-constexpr int kDecWaves = kDecThreads / kWave;
-constexpr int kDecChunk = 512;                  // keys per workgroup
-constexpr int kDecHeads = 16;                   // query heads per KV head the MFMA rows hold
-constexpr int kDecMaxChunks = (kMaxKeyTiles * kBlockN) / kDecChunk;   // chunks of the longest cache
-
-__device__ __forceinline__ float wave_max(float v) {
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
-  return v;
-}
+constexpr int kDecWaves = 8;                        // one 64-key tile per wave
+constexpr int kDecThreads = kDecWaves * kWave;      // 512
+constexpr int kDecChunk = kDecWaves * kBlockN;      // 512 keys per workgroup
+constexpr int kDecHeads = 16;                       // query heads per KV head on the MFMA columns
+constexpr int kCombineThreads = 256;
 
 // Eight int8 codes (one per byte of v) widened to FP16, exactly: with the sign bit flipped a
 // byte b reads as 1024 + 128 + b in the FP16 pattern 0x64xx, and 1152 is then subtracted.
-__device__ __forceinline__ half8 i8x8_to_half8(uint2 v) {
-  const uint32_t lo = v.x ^ 0x80808080u, hi = v.y ^ 0x80808080u;
+__device__ __forceinline__ half8 i8x8_to_half8(uint32_t w0, uint32_t w1) {
   const half2v bias = {(_Float16)-1152.0f, (_Float16)-1152.0f};
   half8 out;
-  const uint32_t w[2] = {lo, hi};
+  const uint32_t w[2] = {w0 ^ 0x80808080u, w1 ^ 0x80808080u};
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     // bytes 0,1 -> halves 0x64b0, 0x64b1; bytes 2,3 -> 0x64b2, 0x64b3
@@ -63,40 +54,92 @@ __device__ __forceinline__ half8 i8x8_to_half8(uint2 v) {
   return out;
 }
 
+// Workgroup = (chunk of 512 keys, KV head, sequence); wave w owns key tile 8 * chunk + w.
+//
+// Scores are computed transposed, S^T = K Q^T, with keys on the 16 rows and the group's query
+// heads on the 16 columns of each tile product.  Score block blk (= 2 * st + h) of a tile puts
+// key 16 * (i / 4) + 4 * blk + i % 4 on row i, so that lane (head, lq) receives the keys
+// 16 * lq + 8 * st + 4 * h + r (r < 4): for each st these are the eight keys 16 * lq + 8 * st + e
+// that the B operand of P.V step st needs in lane (head, lq), slot e.  P therefore never
+// leaves the registers, and the V^T operand of step st is bytes [16 * lq + 8 * st, + 8) of a
+// channel row of the transposed value tile: one 16-byte load per lane covers both steps.
 template <int D>
-__global__ __launch_bounds__(kDecThreads) void decode_partial_kernel(DecodeArgs a) {
-  constexpr int kKeysPerWave = kDecChunk / kDecWaves;   // 128
-  constexpr int kBlocks = kKeysPerWave / 16;             // 16-key score blocks per wave
-  constexpr int kSteps = kKeysPerWave / 32;              // 32-key P.V steps per wave
-  constexpr int kCB = D / 16;                            // 16-channel output blocks
+__global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void decode_partial_kernel(DecodeArgs a) {
+  constexpr int kCB = D / 16;      // 16-channel blocks of the output
+  constexpr int kS16 = D / 32;     // FP16 score products per 16-key block
+  constexpr int kS8 = D / 64;      // INT8 score products per 16-key block
+  constexpr int kQ16 = D + 8, kQ8 = D + 16, kOS = D + 4;   // padded LDS row lengths
   const int chunk = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
   const int G = a.Hq / a.Hk;
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, lq = lane >> 4;
-  __shared__ __align__(16) _Float16 q16[kDecHeads][D];
-  __shared__ __align__(16) int8_t q8[kDecHeads][D];
+  const int n = chunk * kDecWaves + wave;   // key tile of the wave
+  const bool live = n < a.nKB;              // the last chunk may end before its eighth tile
+  __shared__ __align__(16) _Float16 q16[kDecHeads][kQ16];
+  __shared__ __align__(16) int8_t q8[kDecHeads][kQ8];
   __shared__ float cq[kDecHeads];                         // scale * log2(e) * dQ per head
-  // P * dV [head][key] in FP16 for the P.V step, then the waves' partial outputs [wave][head][D]
-  constexpr int kPhBytes = kDecHeads * kDecChunk * 2, kOsumBytes = kDecWaves * kDecHeads * D * 4;
-  __shared__ __align__(16) char buf[kPhBytes > kOsumBytes ? kPhBytes : kOsumBytes];
-  auto ph = reinterpret_cast<_Float16(*)[kDecChunk]>(buf);
-  auto osum = reinterpret_cast<float(*)[kDecHeads][D]>(buf);
-  __shared__ float red[2][kDecWaves][kDecHeads];
+  __shared__ float red_m[kDecWaves][kDecHeads], red_z[kDecWaves][kDecHeads];
+  __shared__ __align__(16) float osum[kDecWaves][kDecHeads][kOS];
 
-  // 1. Query rows of the group: FP16 copy, INT8 codes and FP16-stored scale (Appendix C
+  // 1. The group's query rows (loaded first: the quantization below waits only for them), the
+  //    routing bit and block scales of the tile (Sections 4.2, 4.3), then the key rows of its
+  //    four score blocks on the routed path.  A wave past the last tile reads the last tile
+  //    and masks all of its scores.
+  _Float16 qx[kDecHeads / kDecWaves][D / 64];
+#pragma unroll
+  for (int i = 0; i < kDecHeads / kDecWaves; ++i) {
+    const int g = wave + kDecWaves * i;
+#pragma unroll
+    for (int e = 0; e < D / 64; ++e)
+      qx[i][e] = g < G ? a.Q[((size_t)b * a.Hq + hk * G + g) * D + lane + 64 * e] : (_Float16)0.0f;
+  }
+  const int nt = min(n, a.nKB - 1);
+  const int gj = nt / a.g;
+  const uint64_t word = a.route[((size_t)(a.route_per_batch ? b : 0) * a.Hk + hk) * a.W + (gj >> 6)];
+  const bool int8 = !a.force_fp16 && ((word >> (gj & 63)) & 1ull);
+  const size_t si = ((size_t)b * a.nKB + nt) * a.Hk + hk;
+  const uint16_t dk_bits = a.dK[si], dv_bits = a.dV[si];
+  // K8 and FP16 key rows differ only in their row length (D or 2 D bytes): lane lq reads bytes
+  // 16 * lq + 64 * s of the row for product s of a 16-key block, on either path; the FP16
+  // rows need kS16 products, the K8 rows the first kS8 of them.
+  const char* kbytes = int8 ? reinterpret_cast<const char*>(a.K8) : reinterpret_cast<const char*>(a.K);
+  const size_t row_bytes = int8 ? D : 2 * D;
+  const int kbase = nt * kBlockN + 16 * (l16 >> 2) + (l16 & 3);
+  const char* kp[4];
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk) {
+    const int key = min(kbase + 4 * blk, a.Lk - 1);   // keys past L_k are masked below
+    kp[blk] = kbytes + (((size_t)b * a.Lk + key) * a.Hk + hk) * row_bytes + 16 * lq;
+  }
+  uint4 kr[4][kS16];
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+    for (int s = 0; s < kS8; ++s) kr[blk][s] = ld_global_16(kp[blk] + 64 * s);
+  if (!int8) {
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+      for (int s = kS8; s < kS16; ++s) kr[blk][s] = ld_global_16(kp[blk] + 64 * s);
+  }
+
+  // 2. FP16 copy, INT8 codes and FP16-stored scale of the query rows (Appendix C
   //    quantization; the lone decode row forms its own 128-row block).  Rows past G are 0.
-  for (int g = wave; g < kDecHeads; g += kDecWaves) {
-    const int hq = hk * G + g;
+#pragma unroll
+  for (int i = 0; i < kDecHeads / kDecWaves; ++i) {
+    const int g = wave + kDecWaves * i;
     float x[D / 64];
     float amax = 0.0f;
 #pragma unroll
     for (int e = 0; e < D / 64; ++e) {
-      const _Float16 h = g < G ? a.Q[((size_t)b * a.Hq + hq) * D + lane + 64 * e] : (_Float16)0.0f;
-      q16[g][lane + 64 * e] = h;
-      x[e] = (float)h;
+      q16[g][lane + 64 * e] = qx[i][e];
+      x[e] = (float)qx[i][e];
       amax = fmaxf(amax, fabsf(x[e]));
     }
-    amax = wave_max(amax);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, kWave));
     const float d32 = amax / 127.0f;   // IEEE FP32 division
 #pragma unroll
     for (int e = 0; e < D / 64; ++e) {
@@ -107,146 +150,105 @@ __global__ __launch_bounds__(kDecThreads) void decode_partial_kernel(DecodeArgs 
   }
   __syncthreads();
 
-  // 2. Scores S[head][key] of the wave's 128 keys, 16 keys per block, on the matrix cores:
-  //    v_mfma_i32_16x16x64_i8 (INT8 route) or v_mfma_f32_16x16x32_f16 (FP16 route), heads on
-  //    the rows (A from LDS) and keys on the columns (B straight from the key rows).  Lane l
-  //    holds heads 4*(l/16) + r of key l % 16.
-  i32x4 qa8[D / 64];
-  half8 qa16[D / 32];
-#pragma unroll
-  for (int s = 0; s < D / 64; ++s) qa8[s] = *reinterpret_cast<const i32x4*>(&q8[l16][64 * s + 16 * lq]);
-#pragma unroll
-  for (int s = 0; s < D / 32; ++s) qa16[s] = *reinterpret_cast<const half8*>(&q16[l16][32 * s + 8 * lq]);
-  float cqr[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) cqr[r] = cq[4 * lq + r];
-  const int key_base = chunk * kDecChunk + wave * kKeysPerWave;
-  float sc[kBlocks][4];
-#pragma unroll
-  for (int jb = 0; jb < kBlocks; ++jb) {
-    const int k0 = key_base + 16 * jb;
-    const int n = min(k0 >> 6, a.nKB - 1);   // key tile of the block (clamped past L_k)
-    const int gj = n / a.g;
-    const uint64_t word = a.route[((size_t)(a.route_per_batch ? b : 0) * a.Hk + hk) * a.W + (gj >> 6)];
-    const bool int8 = !a.force_fp16 && ((word >> (gj & 63)) & 1ull);
-    const int key = k0 + l16;
-    const bool valid = key < a.Lk;
-    const size_t row = ((size_t)b * a.Lk + (valid ? key : 0)) * a.Hk + hk;
-    float v[4];
+  // 3. Scores (log2 units) of the wave's 64 keys for the 16 head columns:
+  //    v_mfma_i32_16x16x64_i8 on K8 rows or v_mfma_f32_16x16x32_f16 on FP16 key rows.
+  float sc[4][4];
+  {
     if (int8) {
-      const float dk = half_bits_to_float(a.dK[((size_t)b * a.nKB + n) * a.Hk + hk]);
-      i32x4 acc = {0, 0, 0, 0};
+      i32x4 qb[kS8];
 #pragma unroll
-      for (int s = 0; s < D / 64; ++s) {
-        const i32x4 kb = as_i32x4(ld_global_16(a.K8 + row * D + 64 * s + 16 * lq));
-        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(qa8[s], kb, acc, 0, 0, 0);
+      for (int s = 0; s < kS8; ++s) qb[s] = *reinterpret_cast<const i32x4*>(&q8[l16][64 * s + 16 * lq]);
+      const float f = cq[l16] * half_bits_to_float(dk_bits);
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) {
+        i32x4 acc = {0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < kS8; ++s)
+          acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(as_i32x4(kr[blk][s]), qb[s], acc, 0, 0, 0);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sc[blk][r] = (float)acc[r] * f;
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = (float)acc[r] * (cqr[r] * dk);
     } else {
-      f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+      half8 qb[kS16];
 #pragma unroll
-      for (int s = 0; s < D / 32; ++s) {
-        const half8 kb = as_half8(ld_global_16(a.K + row * D + 32 * s + 8 * lq));
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa16[s], kb, acc, 0, 0, 0);
+      for (int s = 0; s < kS16; ++s) qb[s] = *reinterpret_cast<const half8*>(&q16[l16][32 * s + 8 * lq]);
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) {
+        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int s = 0; s < kS16; ++s)
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(kr[blk][s]), qb[s], acc, 0, 0, 0);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sc[blk][r] = acc[r] * a.scale_log2e;
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = acc[r] * a.scale_log2e;
     }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) sc[jb][r] = (valid && 4 * lq + r < G) ? v[r] : -__builtin_huge_valf();
   }
-
-  // 3. Per-head chunk max and normalizer (the 16 lanes of a quarter-wave share their heads);
-  //    P * dV to LDS in FP16 for the P.V step (the V block scale folded into P).
-  float mx[4];
+  const bool head_ok = l16 < G;   // columns past G are padding
+  float m = -__builtin_huge_valf();
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float m = sc[0][r];
-#pragma unroll
-    for (int jb = 1; jb < kBlocks; ++jb) m = fmaxf(m, sc[jb][r]);
-#pragma unroll
-    for (int x = 1; x < 16; x <<= 1) m = fmaxf(m, __shfl_xor(m, x, kWave));
-    mx[r] = m;
-  }
-  if (l16 == 0) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) red[0][wave][4 * lq + r] = mx[r];
-  }
-  __syncthreads();
-  float zs[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float m = red[0][0][4 * lq + r];
-#pragma unroll
-    for (int w = 1; w < kDecWaves; ++w) m = fmaxf(m, red[0][w][4 * lq + r]);
-    mx[r] = m;
-    zs[r] = 0.0f;
-  }
-#pragma unroll
-  for (int jb = 0; jb < kBlocks; ++jb) {
-    const int t = wave * kKeysPerWave + 16 * jb + l16;           // key within the chunk
-    const int n = min((chunk * kDecChunk + t) >> 6, a.nKB - 1);
-    const float dv = half_bits_to_float(a.dV[((size_t)b * a.nKB + n) * a.Hk + hk]);
+  for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float p = (mx[r] == -__builtin_huge_valf()) ? 0.0f : __builtin_amdgcn_exp2f(sc[jb][r] - mx[r]);
-      zs[r] += p;
-      ph[4 * lq + r][t] = (_Float16)(p * dv);
+      const bool ok = live && head_ok && n * kBlockN + 16 * lq + 4 * blk + r < a.Lk;
+      sc[blk][r] = ok ? sc[blk][r] : -__builtin_huge_valf();
+      m = fmaxf(m, sc[blk][r]);
     }
-  }
+  m = fmaxf(m, __shfl_xor(m, 16, kWave));
+  m = fmaxf(m, __shfl_xor(m, 32, kWave));
+  if (lq == 0) red_m[wave][l16] = m;
+
+  // 4. The transposed V8 tile rows of the wave's P.V products, in flight across the barrier.
+  uint4 vr[kCB];
+  {
+    const int8_t* vt = a.V8 + ((((size_t)b * a.Hk + hk) * a.nKB + nt) * D + l16) * kBlockN + 16 * lq;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float z = zs[r];
-#pragma unroll
-    for (int x = 1; x < 16; x <<= 1) z += __shfl_xor(z, x, kWave);
-    zs[r] = z;
-  }
-  if (l16 == 0) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) red[1][wave][4 * lq + r] = zs[r];
+    for (int cb = 0; cb < kCB; ++cb) vr[cb] = ld_global_16(vt + cb * 16 * kBlockN);
   }
   __syncthreads();
-  if (tid < G) {
-    float z = 0.0f, m = red[0][0][tid];
-#pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) {
-      z += red[1][w][tid];
-      m = fmaxf(m, red[0][w][tid]);
-    }
-    const size_t o = ((size_t)b * a.Hq + hk * G + tid) * a.chunks + chunk;
-    a.part_m[o] = m;
-    a.part_z[o] = z;
-  }
 
-  // 4. O^T[channel][head] += V^T[channel][key] (P dV)^T[key][head], v_mfma_f32_16x16x32_f16:
-  //    A = 8 consecutive keys of one channel from the transposed V8 tile (widened to FP16),
-  //    B = 8 keys of P dV for one head from LDS.  Lane l ends with channels 4*(l/16) + r of
-  //    its 16-channel block for head l % 16.
+  // 5. Chunk max per head; P = 2^(s - m) with the V block scale folded in (FP16 B operand);
+  //    the chunk normalizer sums P before the fold.
+  float mc = red_m[0][l16];
+#pragma unroll
+  for (int w = 1; w < kDecWaves; ++w) mc = fmaxf(mc, red_m[w][l16]);
+  const float dv = half_bits_to_float(dv_bits);
+  half8 pb[2];
+  float z = 0.0f;
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float p = sc[blk][r] == -__builtin_huge_valf() ? 0.0f : __builtin_amdgcn_exp2f(sc[blk][r] - mc);
+      z += p;
+      pb[blk >> 1][4 * (blk & 1) + r] = (_Float16)(p * dv);
+    }
+  z += __shfl_xor(z, 16, kWave);
+  z += __shfl_xor(z, 32, kWave);
+  if (lq == 0) red_z[wave][l16] = z;
+
+  // 6. O^T[channel][head] += V^T[channel][key] (P dV)^T[key][head] on
+  //    v_mfma_f32_16x16x32_f16, V^T widened to FP16 exactly.  Lane (head, lq) ends with
+  //    channels 16 * cb + 4 * lq + r of its head.
   f32x4 acc[kCB];
 #pragma unroll
   for (int cb = 0; cb < kCB; ++cb) acc[cb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-  for (int st = 0; st < kSteps; ++st) {
-    const int kk = wave * kKeysPerWave + 32 * st;                // first key of the step (chunk)
-    const int key0 = chunk * kDecChunk + kk;
-    if (key0 >= a.Lk) break;                                     // the rest of the chunk is past L_k
-    const int n = key0 >> 6;
-    const half8 pb = *reinterpret_cast<const half8*>(&ph[l16][kk + 8 * lq]);
-    const int8_t* vt = a.V8 + ((((size_t)b * a.Hk + hk) * a.nKB + n) * D + l16) * kBlockN +
-                       (key0 & 63) + 8 * lq;
+  {
 #pragma unroll
     for (int cb = 0; cb < kCB; ++cb) {
-      const uint2 raw = *reinterpret_cast<const uint2*>(vt + (size_t)cb * 16 * kBlockN);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(i8x8_to_half8(raw), pb, acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(i8x8_to_half8(vr[cb].x, vr[cb].y), pb[0],
+                                                      acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(i8x8_to_half8(vr[cb].z, vr[cb].w), pb[1],
+                                                      acc[cb], 0, 0, 0);
     }
   }
-  __syncthreads();   // every wave is done reading P before the buffer holds outputs
+  if (head_ok) {
 #pragma unroll
-  for (int cb = 0; cb < kCB; ++cb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) osum[wave][l16][16 * cb + 4 * lq + r] = acc[cb][r];
+    for (int cb = 0; cb < kCB; ++cb)
+      *reinterpret_cast<f32x4*>(&osum[wave][l16][16 * cb + 4 * lq]) = acc[cb];
+  }
   __syncthreads();
+
+  // 7. Sum of the eight waves: (max, normalizer, unnormalized output) of the chunk per head.
   for (int o = tid; o < G * D; o += kDecThreads) {
     const int g = o / D, c = o % D;
     float sum = 0.0f;
@@ -254,55 +256,86 @@ __global__ __launch_bounds__(kDecThreads) void decode_partial_kernel(DecodeArgs 
     for (int w = 0; w < kDecWaves; ++w) sum += osum[w][g][c];
     a.part_o[(((size_t)b * a.Hq + hk * G + g) * a.chunks + chunk) * D + c] = sum;
   }
+  if (tid < G) {
+    float zz = 0.0f, mm = red_m[0][tid];
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+      zz += red_z[w][tid];
+      mm = fmaxf(mm, red_m[w][tid]);
+    }
+    const size_t o = ((size_t)b * a.Hq + hk * G + tid) * a.chunks + chunk;
+    a.part_m[o] = mm;
+    a.part_z[o] = zz;
+  }
 }
 
-// One workgroup per (sequence, query head): the chunks' maxima give m; each chunk's weight
-// 2^(m_i - m) goes to LDS with the normalizer z = sum z_i 2^(m_i - m); then threads over
-// (channel, chunk residue) add the weighted chunk outputs and the residues are summed in LDS.
+// One workgroup per (sequence, query head).  Thread (part, c4) owns channels 4*c4 .. 4*c4+3
+// and the chunks part, part + kRows, ...; it keeps a running (max, normalizer, output) merged
+// with the log-sum-exp rule, loading kUnroll chunks ahead.  The parts are merged in LDS.
 template <int D>
-__global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(DecodeArgs a) {
-  constexpr int kParts = kDecThreads / D;
+__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeArgs a) {
+  constexpr int kLanes = D / 4;                     // float4 lanes per chunk row
+  constexpr int kRows = kCombineThreads / kLanes;   // chunk rows per pass
+  constexpr int kUnroll = 8;
   const int bh = blockIdx.x;   // b * Hq + hq
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid >> 6;
-  __shared__ float wgt[kDecMaxChunks];
-  __shared__ float red[kDecWaves];
-  __shared__ float opart[kParts][D];
+  const int tid = threadIdx.x, c4 = tid % kLanes, part = tid / kLanes;
+  __shared__ float sm[kRows], sz[kRows];
+  __shared__ f32x4 so[kRows][kLanes];
   const float* pm = a.part_m + (size_t)bh * a.chunks;
   const float* pz = a.part_z + (size_t)bh * a.chunks;
-  float m = -__builtin_huge_valf();
-  for (int i = tid; i < a.chunks; i += kDecThreads) m = fmaxf(m, pm[i]);
-  m = wave_max(m);
-  if (lane == 0) red[wave] = m;
-  __syncthreads();
-  m = red[0];
+  const f32x4* po = reinterpret_cast<const f32x4*>(a.part_o + (size_t)bh * a.chunks * D) + c4;
+  const float ninf = -__builtin_huge_valf();
+  float m = ninf, z = 0.0f;
+  f32x4 o = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int i0 = part; i0 < a.chunks; i0 += kRows * kUnroll) {
+    float mi[kUnroll], zi[kUnroll];
+    f32x4 oi[kUnroll];
 #pragma unroll
-  for (int w = 1; w < kDecWaves; ++w) m = fmaxf(m, red[w]);
-  float zl = 0.0f;
-  for (int i = tid; i < a.chunks; i += kDecThreads) {
-    const float f = (m == -__builtin_huge_valf() || pm[i] == -__builtin_huge_valf())
-                        ? 0.0f : __builtin_amdgcn_exp2f(pm[i] - m);
-    wgt[i] = f;
-    zl += pz[i] * f;
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = i0 + u * kRows;
+      const bool ok = i < a.chunks;
+      mi[u] = ok ? pm[i] : ninf;
+      zi[u] = ok ? pz[i] : 0.0f;
+      oi[u] = ok ? po[(size_t)i * kLanes] : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    float mn = m;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) mn = fmaxf(mn, mi[u]);
+    if (mn == ninf) continue;
+    const float f = m == ninf ? 0.0f : __builtin_amdgcn_exp2f(m - mn);
+    z *= f;
+    o *= f;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const float fu = mi[u] == ninf ? 0.0f : __builtin_amdgcn_exp2f(mi[u] - mn);
+      z += zi[u] * fu;
+      o += oi[u] * fu;
+    }
+    m = mn;
   }
-  zl = wave_sum(zl);
-  __syncthreads();   // red is reused
-  if (lane == 0) red[wave] = zl;
+  if (c4 == 0) {
+    sm[part] = m;
+    sz[part] = z;
+  }
+  so[part][c4] = o;
   __syncthreads();
-  float z = 0.0f;
+  if (tid < kLanes) {
+    float mm = sm[0];
 #pragma unroll
-  for (int w = 0; w < kDecWaves; ++w) z += red[w];
-  const int c = tid % D, part = tid / D;
-  const float* po = a.part_o + (size_t)bh * a.chunks * D + c;
-  float o = 0.0f;
-#pragma unroll 4
-  for (int i = part; i < a.chunks; i += kParts) o += po[(size_t)i * D] * wgt[i];
-  opart[part][c] = o;
-  __syncthreads();
-  if (tid < D) {
-    float t = 0.0f;
+    for (int p = 1; p < kRows; ++p) mm = fmaxf(mm, sm[p]);
+    float zz = 0.0f;
+    f32x4 oo = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int r = 0; r < kParts; ++r) t += opart[r][tid];
-    a.O[(size_t)bh * D + tid] = (_Float16)(z > 0.0f ? t / z : 0.0f);
+    for (int p = 0; p < kRows; ++p) {
+      const float fp = sm[p] == ninf ? 0.0f : __builtin_amdgcn_exp2f(sm[p] - mm);
+      zz += sz[p] * fp;
+      oo += so[p][tid] * fp;
+    }
+    const float inv = zz > 0.0f ? 1.0f / zz : 0.0f;
+    half4 h;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) h[r] = (_Float16)(oo[r] * inv);
+    *reinterpret_cast<half4*>(a.O + (size_t)bh * D + 4 * tid) = h;
   }
 }
 
@@ -311,7 +344,7 @@ hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t stream) {
   if (a.Hq / a.Hk > kDecHeads) return hipErrorInvalidValue;
   hipLaunchKernelGGL((decode_partial_kernel<D>), dim3(a.chunks, a.Hk, a.B), dim3(kDecThreads), 0,
                      stream, a);
-  hipLaunchKernelGGL(decode_combine_kernel<D>, dim3(a.B * a.Hq), dim3(kDecThreads), 0, stream, a);
+  hipLaunchKernelGGL(decode_combine_kernel<D>, dim3(a.B * a.Hq), dim3(kCombineThreads), 0, stream, a);
   return hipGetLastError();
 }
 
