@@ -46,7 +46,8 @@ __device__ __forceinline__ SeqRows seq_rows(const int* seqs, int b, int L, int n
 }
 
 // TRANSPOSED (64-row blocks only): the codes of block r of head h go out as one [D][64] tile,
-// [B, H, nblk, D, 64], rows past the sequence end as 0 (the INT8 value-cache layout of decode).
+// [B, H, nblk, D, 64], rows past the sequence end as 0 (the INT8 value-cache layout of decode);
+// the tile is transposed in LDS and written in 16-byte runs.
 template <int D, int BLK, bool TRANSPOSED = false>
 __global__ __launch_bounds__(kPrepThreads) void quantize_blocks_kernel(
     const _Float16* __restrict__ X, int8_t* __restrict__ X8, uint16_t* __restrict__ dX,
@@ -55,6 +56,8 @@ __global__ __launch_bounds__(kPrepThreads) void quantize_blocks_kernel(
   constexpr int kPer = BLK * kChunksPerRow / kPrepThreads;      // chunks per thread
   static_assert(kPer * kPrepThreads == BLK * kChunksPerRow, "block split");
   __shared__ float red[kPrepThreads / kWave];
+  // TRANSPOSED: the block's codes as [D][BLK] (rows padded to keep 16-byte alignment)
+  __shared__ __align__(16) uint8_t tile[TRANSPOSED ? D : 1][TRANSPOSED ? BLK + 16 : 16];
 
   const int r = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const SeqRows sq = seq_rows(seqs, b, L, nblk, f_start, f_len, f_blk);
@@ -98,17 +101,24 @@ __global__ __launch_bounds__(kPrepThreads) void quantize_blocks_kernel(
         }
       }
       if constexpr (TRANSPOSED) {
-        int8_t* t = X8 + (((size_t)b * H + h) * nblk + r) * (size_t)(D * BLK) + (size_t)(ch * 8) * BLK + row;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) t[e * BLK] = (int8_t)(packed[e >> 2] >> (8 * (e & 3)));
+        for (int e = 0; e < 8; ++e) tile[ch * 8 + e][row] = (uint8_t)(packed[e >> 2] >> (8 * (e & 3)));
       } else {
         const size_t off = ((size_t)(sq.start + row0 + row) * H + h) * D + ch * 8;
         *reinterpret_cast<uint2*>(X8 + off) = make_uint2(packed[0], packed[1]);
       }
     } else if constexpr (TRANSPOSED) {   // padding keys of the last tile
-      int8_t* t = X8 + (((size_t)b * H + h) * nblk + r) * (size_t)(D * BLK) + (size_t)(ch * 8) * BLK + row;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) t[e * BLK] = 0;
+      for (int e = 0; e < 8; ++e) tile[ch * 8 + e][row] = 0;
+    }
+  }
+  if constexpr (TRANSPOSED) {   // the [D][64] tile out in 16-byte runs
+    __syncthreads();
+    int8_t* t = X8 + (((size_t)b * H + h) * nblk + r) * (size_t)(D * BLK);
+    for (int k = threadIdx.x; k < D * BLK / 16; k += kPrepThreads) {
+      const int c = k / (BLK / 16), j = k % (BLK / 16);
+      *reinterpret_cast<uint4*>(t + (size_t)c * BLK + 16 * j) =
+          *reinterpret_cast<const uint4*>(&tile[c][16 * j]);
     }
   }
   if (threadIdx.x == 0) {
