@@ -15,6 +15,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import statistics
 import json
 import math
 import os
@@ -275,6 +276,10 @@ def main(argv=None):
         "attention_ms": round(attn_avg, 4),
         "deviation_vs_fp16": {k2: float(f"{v2:.4e}") for k2, v2 in deviation.items()},
         "prepare_ms": round(prep_avg, 4),
+        "timing_ms": {"step_median": round(statistics.median(step_ms), 4),
+                      "step_min": round(min(step_ms), 4),
+                      "attention_median": round(statistics.median(attn_ms), 4),
+                      "attention_min": round(min(attn_ms), 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": round(peak, 2),
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                      "traffic": recorded_traffic(cfg.name),
