@@ -312,16 +312,8 @@ def bench_decode(args, cfg, mask):
     q1, k, v = to(Q[:, -1:]), to(K), to(V)
     del Q
     K8, dK, V8, dV = tm.tilemix_quantize_kv(k, v)
-    T_mask = -(-(-(-cfg.L // cfg.block_n)) // cfg.group_size)
-    rng = np.random.default_rng(cfg.seed)
-    if mask.kind == "all_fp16":
-        R = np.zeros((cfg.Hk, 1, T_mask), np.uint8)
-    elif mask.kind == "all_int8":
-        R = np.ones((cfg.Hk, 1, T_mask), np.uint8)
-    else:
-        R = (rng.random((cfg.Hk, 1, T_mask)) < (mask.p_int8 or 0.5)).astype(np.uint8)
-    from synth import pack_route_bits
-    words = pack_route_bits(R)
+    from synth import decode_route_bits
+    words, R = decode_route_bits(cfg, mask)
     w = to(words.view(np.int64))
     hint = 0 if mask.kind == "all_fp16" else -1
     p = tm.Params(cfg.B, cfg.Hq, cfg.Hk, 1, cfg.L, cfg.d, cfg.block_m, cfg.block_n,

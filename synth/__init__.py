@@ -9,6 +9,7 @@ from .configs import WorkloadConfig, MaskSpec, WORKLOADS, workload, small_worklo
 from .generate import (
     make_qkv,
     make_route_bits,
+    decode_route_bits,
     legal_group_table,
     route_stats,
     sample_rows,
@@ -23,6 +24,7 @@ __all__ = [
     "small_workload",
     "make_qkv",
     "make_route_bits",
+    "decode_route_bits",
     "legal_group_table",
     "route_stats",
     "sample_rows",

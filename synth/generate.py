@@ -153,6 +153,21 @@ def make_route_bits(cfg: WorkloadConfig, mask: MaskSpec | None = None, mask_inde
     return pack_route_bits(R), R
 
 
+def decode_route_bits(cfg: WorkloadConfig, mask: MaskSpec):
+    """Routing map of one decode step over the workload's L keys: one query-tile row per KV
+    head, all FP16 / all INT8 / Bernoulli(p_int8, default 0.5) per key group, broadcast over
+    sequences.  Return (packed words [1, H_k, 1, W], 0/1 map [H_k, 1, T_mask])."""
+    T_mask = -(-(-(-cfg.L // cfg.block_n)) // cfg.group_size)
+    if mask.kind == "all_fp16":
+        R = np.zeros((cfg.Hk, 1, T_mask), np.uint8)
+    elif mask.kind == "all_int8":
+        R = np.ones((cfg.Hk, 1, T_mask), np.uint8)
+    else:
+        rng = np.random.default_rng(cfg.seed)
+        R = (rng.random((cfg.Hk, 1, T_mask)) < (mask.p_int8 or 0.5)).astype(np.uint8)
+    return pack_route_bits(R), R
+
+
 def route_stats(cfg: WorkloadConfig, R: np.ndarray) -> dict:
     """Realized INT8 coverage: over legal groups (rho_hat) and over legal pairs (rho_p)."""
     legal = legal_group_table(cfg)

@@ -107,3 +107,28 @@ def test_debug_and_quantize_reject_before_launch():
     assert lib.tilemix_debug_qk_int32(ctypes.byref(cp), ok, ok, ok, -1, ok, None) == 2
     assert lib.tilemix_debug_qk_int32(ctypes.byref(cp), ok, ok, ok, 0, ok, None) == 0   # nothing to do
     assert lib.tilemix_quantize(ctypes.byref(cp), None, ok, ok, ok, ok, ok, None) == 1
+
+
+def test_decode_rejects_before_launch():
+    # Every call below fails a host-side check, so no kernel is launched (the pointers are fake).
+    lib = tm.load_library()
+    ok = ctypes.c_void_p(0x100000)
+    dp = dict(len_q=1, len_k=5000, heads_q=64, heads_kv=8, group_size=8)
+
+    def call(cp, ptr=ok, ws=None, ws_bytes=1 << 40):
+        return lib.tilemix_decode(ctypes.byref(cp.c()), ptr, ptr, ptr, ptr, ptr, ptr, ptr, ptr, ws,
+                                  ws_bytes, None)
+
+    assert call(_cp(**dp)) == 5                                  # shapes pass; no workspace
+    assert call(_cp(**dict(dp, len_q=2))) == 3                   # one query token only
+    assert call(_cp(**dict(dp, heads_q=136, heads_kv=8))) == 3   # G = 17 > 16
+    assert call(_cp(**dict(dp, len_k=262145))) == 3              # past the longest cache
+    assert call(_cp(**dict(dp, len_k=262144))) == 5
+    assert call(_cp(**dp), ptr=None) == 1
+    assert call(_cp(**dp), ptr=ctypes.c_void_p(0x1001)) == 4
+    assert call(_cp(**dp), ws=ctypes.c_void_p(0x100080)) == 4
+    # partial results: B * H_q * ceil(L_k / 512) chunks of (max, normalizer, d floats)
+    need = tm.tilemix_decode_workspace_size(_cp(**dp))
+    assert need >= 64 * 10 * (2 + 128) * 4
+    assert call(_cp(**dp), ws=ok, ws_bytes=need - 1) == 5
+    assert b"needed" in lib.tilemix_last_error()

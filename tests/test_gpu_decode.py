@@ -67,3 +67,70 @@ def test_decode_parity(B, Hq, Hk, d, Lk, g, rpb):
         rel = float(np.sqrt((diff ** 2).sum() / (ref ** 2).sum()))
         log(f"  max_abs={mx:.3e} rel_l2={rel:.3e}")
         assert mx <= MAX_ABS and rel <= REL_L2, (p, mx, rel)
+
+
+def _check(got, ref, what):
+    diff = got - ref
+    mx = float(np.abs(diff).max())
+    rel = float(np.sqrt((diff ** 2).sum() / (ref ** 2).sum()))
+    log(f"  {what}: max_abs={mx:.3e} rel_l2={rel:.3e}")
+    assert mx <= MAX_ABS and rel <= REL_L2, (what, mx, rel)
+
+
+@pytest.mark.timeout(600)
+def test_decode_full_workload_sampled():
+    """The 64K-key, B = 4, 64/8-head decode step bench.py times, with its three routing maps:
+    every query head of sampled (sequence, KV head) groups against the oracle."""
+    import torch
+    import paper_2608_17336_amd as tm
+    from synth import WORKLOADS, decode_route_bits
+    cfg = WORKLOADS["64k-b4-gqa"]
+    log(f"decode {cfg.name}: generating inputs")
+    Q, K, V = make_qkv(cfg)
+    Q1 = np.ascontiguousarray(Q[:, -1:])
+    del Q
+    k, v = to_dev(K), to_dev(V)
+    K8, dK, V8, dV = tm.tilemix_quantize_kv(k, v)
+    G = cfg.Hq // cfg.Hk
+    picks = [(0, 0), (cfg.B - 1, cfg.Hk - 1), (cfg.B // 2, 3)]
+    # the oracle's cache of each picked (sequence, KV head) slice (quantization is per slice)
+    caches = {(b, hk): kv_cache(K[b:b + 1, :, hk:hk + 1], V[b:b + 1, :, hk:hk + 1]) for b, hk in picks}
+    q1 = to_dev(Q1)
+    for mask in cfg.masks:
+        words, _ = decode_route_bits(cfg, mask)
+        hint = 0 if mask.kind == "all_fp16" else -1
+        log(f"  mask={mask.label}: GPU")
+        O = tm.tilemix_decode(q1, k, K8, dK, V8, dV, to_dev(words), cfg.group_size, cfg.scale,
+                              route_hint=hint)
+        torch.cuda.synchronize()
+        got = O.float().cpu().numpy().astype(np.float64)
+        for b, hk in picks:
+            ref = routed_decode(Q1[b:b + 1, :, hk * G:(hk + 1) * G], K[b:b + 1, :, hk:hk + 1],
+                                *caches[(b, hk)], words[:, hk:hk + 1], cfg.group_size, cfg.scale)
+            _check(got[b:b + 1, :, hk * G:(hk + 1) * G], ref, f"{mask.label} b={b} hk={hk}")
+
+
+@pytest.mark.timeout(300)
+def test_decode_longest_cache_full_group():
+    """L_k = 262144 (the longest cache the build supports: 512 chunks to merge) with a
+    16-head GQA group (every matrix-core column used), g = 16 (four routing words)."""
+    import torch
+    import paper_2608_17336_amd as tm
+    Lk, g = 262144, 16
+    cfg = small_workload("declong", B=1, Hq=16, Hk=1, d=128, L=Lk, group_size=g, k_outliers=True,
+                         index=977)
+    log(f"decode L_k={Lk} G=16 g={g}: generating inputs")
+    Q, K, V = make_qkv(cfg)
+    Q1 = np.ascontiguousarray(Q[:, -1:])
+    del Q
+    k, v = to_dev(K), to_dev(V)
+    K8, dK, V8, dV = tm.tilemix_quantize_kv(k, v)
+    ck = kv_cache(K, V)
+    T_mask = -(-(-(-Lk // 64)) // g)
+    R = (np.random.default_rng(977).random((1, 1, T_mask)) < 0.5).astype(np.uint8)
+    words = pack_route_bits(R)
+    assert words.shape[-1] == 4
+    O = tm.tilemix_decode(to_dev(Q1), k, K8, dK, V8, dV, to_dev(words), g, cfg.scale)
+    torch.cuda.synchronize()
+    got = O.float().cpu().numpy().astype(np.float64)
+    _check(got, routed_decode(Q1, K, *ck, words, g, cfg.scale), "L_k=262144")
