@@ -129,6 +129,9 @@ def main(argv=None):
     ap.add_argument("--decode", action="store_true",
                     help="time one decode step over an INT8 key/value cache of the workload's "
                          "shape (L_k = L, one query token per sequence)")
+    ap.add_argument("--fused", action="store_true",
+                    help="time the fused on-the-fly operand mode (tilemix_prefill_fused: no Q8/K8 "
+                         "scratch, quantization on chip) instead of quantize-once")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 256 MiB device copy (HBM counter calibration)")
     args = ap.parse_args(argv)
@@ -187,17 +190,23 @@ def main(argv=None):
               scale=cfg.scale, route_hint=hint)
     p = tm.Params(cfg.B, cfg.Hq, cfg.Hk, cfg.L, cfg.L, cfg.d, cfg.block_m, cfg.block_n,
                   cfg.group_size, cfg.causal, cfg.scale, False, hint)
-    ws = torch.empty(tm.tilemix_workspace_size(p), dtype=torch.uint8, device=dev)
+    ws_bytes = tm.tilemix_fused_workspace_size(p) if args.fused else tm.tilemix_workspace_size(p)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     O = torch.empty((cfg.B, cfg.L, cfg.Hq, cfg.d), dtype=torch.float16, device=dev)
     stream = torch.cuda.current_stream()
 
     def step(e0=None, e1=None, e2=None):
         if e0 is not None:
             e0.record(stream)
-        tm.tilemix_prepare(q, k, v, workspace=ws, stream=stream, **kw)
-        if e1 is not None:
-            e1.record(stream)
-        tm.tilemix_attend(q, k, w, ws, O=O, stream=stream, **kw)
+        if args.fused:   # one call: V tiles, then the kernel that quantizes on chip
+            if e1 is not None:
+                e1.record(stream)
+            tm.tilemix_prefill_fused(q, k, v, w, workspace=ws, O=O, stream=stream, **kw)
+        else:
+            tm.tilemix_prepare(q, k, v, workspace=ws, stream=stream, **kw)
+            if e1 is not None:
+                e1.record(stream)
+            tm.tilemix_attend(q, k, w, ws, O=O, stream=stream, **kw)
         if e2 is not None:
             e2.record(stream)
 
@@ -234,8 +243,11 @@ def main(argv=None):
     # the FP16 route (untimed).
     O16 = torch.empty_like(O)
     kw16 = dict(kw, route_hint=0)
-    tm.tilemix_prepare(q, k, v, workspace=ws, stream=stream, **kw16)
-    tm.tilemix_attend(q, k, w, ws, O=O16, stream=stream, **kw16)
+    if args.fused:
+        tm.tilemix_prefill_fused(q, k, v, w, workspace=ws, O=O16, stream=stream, **kw16)
+    else:
+        tm.tilemix_prepare(q, k, v, workspace=ws, stream=stream, **kw16)
+        tm.tilemix_attend(q, k, w, ws, O=O16, stream=stream, **kw16)
     torch.cuda.synchronize()
     ss = sa = ref = 0.0
     mx = 0.0
@@ -271,6 +283,7 @@ def main(argv=None):
         "config": {"workload": cfg.name, "B": cfg.B, "Hq": cfg.Hq, "Hk": cfg.Hk, "d": cfg.d,
                    "L": cfg.L, "causal": cfg.causal, "tile": f"{cfg.block_m}x{cfg.block_n}",
                    "group_size": cfg.group_size, "mask": mask_label,
+                   "operands": "fused on-the-fly" if args.fused else "quantize-once",
                    "rho_hat": round(stats["rho_hat"], 4), "rho_pairs": round(stats["rho_pairs"], 4)},
         "pct_of_weighted_roofline": round(100.0 * fm["t_star_s"] / (ms_per_step * 1e-3), 2),
         "attention_ms": round(attn_avg, 4),
@@ -282,8 +295,9 @@ def main(argv=None):
                       "attention_min": round(min(attn_ms), 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": round(peak, 2),
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                     "traffic": recorded_traffic(cfg.name),
-                     "kernel": f"routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1>",
+                     "traffic": None if args.fused else recorded_traffic(cfg.name),
+                     "kernel": (f"v_tiles_kernel + routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1, true>"
+                                if args.fused else f"routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1>"),
                      "peak_note": "precision-weighted: QK^T FP16 share at 2.5 PFLOP/s, INT8 share at "
                                   "5.0 POP/s, P.V at 2.5 PFLOP/s"},
     }

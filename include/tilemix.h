@@ -106,6 +106,25 @@ tilemix_status tilemix_prefill(const tilemix_params* params,
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * tilemix_prefill_fused -- tilemix_prefill in the fused on-the-fly operand mode (Appendix D,
+ * "Storage and Execution Layout", the fused on-the-fly mode; Appendix C quantization rules):
+ * no Q8 / K8 / scale tensors and no quantization pass.  The kernel computes the scales and
+ * codes on chip, only for what INT8-routed groups use: each workgroup quantizes the 128-row
+ * query block of its rows once, and every INT8-routed 64-key tile (one key scale block) after
+ * its FP16 copy reaches LDS.  Codes and scales equal those of tilemix_quantize, so the output
+ * equals tilemix_prefill's bit for bit.  Arguments as in tilemix_prefill; the workspace
+ * (tilemix_fused_workspace_size bytes) holds only V laid out per 64-key tile.  The INT8 route
+ * costs more per tile here (every workgroup requantizes the key tiles it reads); the mode
+ * trades that time for the Q8 / K8 scratch.
+ */
+tilemix_status tilemix_fused_workspace_size(const tilemix_params* params, size_t* bytes);
+
+tilemix_status tilemix_prefill_fused(const tilemix_params* params,
+                                     const void* Q, const void* K, const void* V,
+                                     const uint64_t* route_bits, void* O,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * tilemix_prepare -- the first half of tilemix_prefill: the quantize-once pass (Q8, K8 and
  * their FP16 block scales, Appendix C "Quantize-Once Execution"; skipped when route_hint is 0)
  * and the per-64-key-tile V layout, written into `workspace`.  Arguments as in

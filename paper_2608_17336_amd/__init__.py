@@ -22,6 +22,8 @@ __all__ = [
     "tilemix_route_words_per_row",
     "tilemix_workspace_size",
     "tilemix_prefill",
+    "tilemix_fused_workspace_size",
+    "tilemix_prefill_fused",
     "tilemix_prepare",
     "tilemix_attend",
     "tilemix_quantize",
@@ -45,6 +47,8 @@ EXPORTED_SYMBOLS = (
     "tilemix_route_words_per_row",
     "tilemix_workspace_size",
     "tilemix_prefill",
+    "tilemix_fused_workspace_size",
+    "tilemix_prefill_fused",
     "tilemix_prepare",
     "tilemix_attend",
     "tilemix_quantize",
@@ -188,6 +192,10 @@ def load_library() -> ctypes.CDLL:
     lib.tilemix_workspace_size.restype = ctypes.c_int
     lib.tilemix_prefill.argtypes = [P, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.tilemix_prefill.restype = ctypes.c_int
+    lib.tilemix_fused_workspace_size.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+    lib.tilemix_fused_workspace_size.restype = ctypes.c_int
+    lib.tilemix_prefill_fused.argtypes = [P, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.tilemix_prefill_fused.restype = ctypes.c_int
     lib.tilemix_prepare.argtypes = [P, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.tilemix_prepare.restype = ctypes.c_int
     lib.tilemix_attend.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
@@ -283,9 +291,9 @@ def _check_inputs(p: Params, Q, K, V=None):
         _require(V, torch.float16, (p.batch, p.len_k, p.heads_kv, p.head_dim), "V")
 
 
-def _workspace(p: Params, workspace, device):
+def _workspace(p: Params, workspace, device, fused: bool = False):
     import torch
-    need = tilemix_workspace_size(p)
+    need = tilemix_fused_workspace_size(p) if fused else tilemix_workspace_size(p)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=device)
     nbytes = workspace.numel() * workspace.element_size()
@@ -318,6 +326,29 @@ def tilemix_prefill(Q, K, V, route_bits, group_size: int, tile=(128, 64), causal
     workspace, nbytes = _workspace(p, workspace, Q.device)
     cp = p.c()
     _check(load_library().tilemix_prefill(
+        ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace),
+        ctypes.c_size_t(nbytes), _stream(stream)))
+    return O
+
+
+def tilemix_fused_workspace_size(params: Params) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().tilemix_fused_workspace_size(ctypes.byref(params.c()), ctypes.byref(n)))
+    return n.value
+
+
+def tilemix_prefill_fused(Q, K, V, route_bits, group_size: int, tile=(128, 64), causal: bool = True,
+                          scale: float | None = None, *, O=None, workspace=None, stream=None,
+                          route_per_batch: bool = False, route_hint: int = -1):
+    """Routed prefill attention in the fused on-the-fly operand mode (no Q8/K8 scratch; the
+    kernel quantizes on chip).  Arguments and result as tilemix_prefill; ``workspace`` (uint8,
+    >= tilemix_fused_workspace_size) is allocated when not given."""
+    p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
+    _check_inputs(p, Q, K, V)
+    O = _route_and_out(p, Q, route_bits, O)
+    workspace, nbytes = _workspace(p, workspace, Q.device, fused=True)
+    cp = p.c()
+    _check(load_library().tilemix_prefill_fused(
         ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace),
         ctypes.c_size_t(nbytes), _stream(stream)))
     return O

@@ -343,14 +343,23 @@ __device__ __forceinline__ void exp_pair(const f32x16& x0, const f32x16& x1, flo
   pfr[t][e + 1] = pr[1];
 }
 
-template <int D, int BM, int HEADS>
+// OTF: the fused on-the-fly operand mode (Appendix D, "Storage and Execution Layout"): no Q8 /
+// K8 / scale tensors exist.  The workgroup quantizes its query block on chip in the prologue
+// (a 128-row Q block is one or two workgroups' rows) and every INT8-routed key tile after its
+// FP16 copy lands: the tile's absmax, scale and codes (the 64-key tile is exactly one key
+// scale block) into an INT8 slot in the K8 layout, for the same INT8 products.
+template <int D, int BM, int HEADS, bool OTF = false>
 __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) {
   using C = TileCfg<D, BM, HEADS>;
+  static_assert(!OTF || HEADS == 1, "on-the-fly operands: one query head per workgroup");
   // Two K slots and two V slots: step n reads K of tile n + 1 and V of tile n while K of tile
   // n + 2 and V of tile n + 1 are copied into the slots that step n - 1 released.  72 KB at
   // d = 128, so two workgroups share a CU and each SIMD runs one wave of each.
-  __shared__ __align__(16) char smem[2 * C::kKBytes + 2 * C::kVBytes];
-  __shared__ uint16_t key_scale[kMaxKeyTiles];   // dK of this row's key tiles (FP16 bits)
+  // OTF: one INT8 key slot after the K and V slots (the key scales come from the chip).
+  constexpr int kK8Off = 2 * C::kKBytes + 2 * C::kVBytes;
+  __shared__ __align__(16) char smem[kK8Off + (OTF ? C::kK8Bytes : 0)];
+  __shared__ uint16_t key_scale[OTF ? 1 : kMaxKeyTiles];   // dK of this row's key tiles (FP16 bits)
+  __shared__ float otf_red[OTF ? C::kWaves : 1];          // OTF: per-wave absmax partials
 
   int b, hq0, hk, m;
   decode_unit<HEADS>(blockIdx.x, a.B, a.Hq, a.Hk, a.T_m, b, hq0, hk, m);
@@ -434,13 +443,94 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     qf[s] = (need_fp16 && row_ok) ? as_half8(ld_global_16(a.Q + qoff + 16 * s + 8 * hi)) : half8{};
 #pragma unroll
   for (int s = 0; s < D / 32; ++s)
-    q8f[s] = (need_int8 && row_ok) ? as_i32x4(ld_global_16(a.Q8 + qoff + 32 * s + 16 * hi)) : i32x4{};
-  const float dq = (need_int8 && wave_active)
-                       ? load_scale_uniform(a.dQ, (size_t)(qblk0 + q0 / kQuantBlockQ) * a.Hq + hq)
-                       : 0.0f;
+    q8f[s] = (!OTF && need_int8 && row_ok) ? as_i32x4(ld_global_16(a.Q8 + qoff + 32 * s + 16 * hi))
+                                           : i32x4{};
+  float dq = (!OTF && need_int8 && wave_active)
+                 ? load_scale_uniform(a.dQ, (size_t)(qblk0 + q0 / kQuantBlockQ) * a.Hq + hq)
+                 : 0.0f;
+
+  // OTF: maximum of a per-thread value over the workgroup (every thread gets it).
+  auto wg_max = [&](float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    if (lane == 0) otf_red[wave] = v;
+    __syncthreads();
+    float r = otf_red[0];
+#pragma unroll
+    for (int w = 1; w < C::kWaves; ++w) r = fmaxf(r, otf_red[w]);
+    return r;
+  };
+  // OTF: the code of x in a block with scale d32 = absmax / 127 and rcp = 1 / d32 (both
+  // correctly rounded), as the low byte of the returned word.  x * rcp refined by one residual
+  // step is the correctly rounded x / d32 (checked exhaustively over every FP16 x and block
+  // absmax), the same quotient the quantize-once pass divides out; adding 1.5 * 2^23 rounds it
+  // half to even into the low mantissa bits.  |x| <= absmax keeps the quotient within
+  // 127 * (1 + 2^-23), so the clamp to [-127, 127] of the quantization rule never acts.
+  auto code_word = [](float x, float d32, float rcp) {
+    const float q0 = fmaf(x, rcp, 0.0f);   // x * rcp (an FMA takes x in FP16 directly)
+    const float q = fmaf(fmaf(-q0, d32, x), rcp, q0);
+    return __builtin_bit_cast(uint32_t, q + 12582912.0f);
+  };
+  // Low bytes of four code words, packed little-endian.
+  auto pack4 = [](uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+    const uint32_t lo = __builtin_amdgcn_perm(w1, w0, 0x0c0c0400u);
+    const uint32_t hi = __builtin_amdgcn_perm(w3, w2, 0x0c0c0400u);
+    return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+  };
+  // Largest |h| of eight FP16 values, as FP16 bits: finite non-negative FP16 values order like
+  // their bit patterns, so packed unsigned 16-bit maxima of the magnitudes serve.
+  auto absmax_bits = [](uint4 v, uint32_t m) {
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+    u16x2 acc = __builtin_bit_cast(u16x2, m);
+    acc = __builtin_elementwise_max(acc, __builtin_bit_cast(u16x2, v.x & 0x7fff7fffu));
+    acc = __builtin_elementwise_max(acc, __builtin_bit_cast(u16x2, v.y & 0x7fff7fffu));
+    acc = __builtin_elementwise_max(acc, __builtin_bit_cast(u16x2, v.z & 0x7fff7fffu));
+    acc = __builtin_elementwise_max(acc, __builtin_bit_cast(u16x2, v.w & 0x7fff7fffu));
+    return __builtin_bit_cast(uint32_t, acc);
+  };
+  auto bits_max_float = [](uint32_t m) {
+    return half_bits_to_float((uint16_t)max(m & 0xffffu, m >> 16));
+  };
+  // 16 codes of the FP16 values in two 16-byte granules.
+  auto codes16 = [&](uint4 g0, uint4 g1, float d32, float rcp) {
+    const half8 h0 = as_half8(g0), h1 = as_half8(g1);
+    uint32_t w[16];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      w[e] = code_word((float)h0[e], d32, rcp);
+      w[8 + e] = code_word((float)h1[e], d32, rcp);
+    }
+    return make_uint4(pack4(w[0], w[1], w[2], w[3]), pack4(w[4], w[5], w[6], w[7]),
+                      pack4(w[8], w[9], w[10], w[11]), pack4(w[12], w[13], w[14], w[15]));
+  };
+  if constexpr (OTF) {
+    if (need_int8) {   // the same for every wave of the workgroup
+      // Q block of this row: rows qb0 .. qb0 + 127 of the sequence (those that exist).
+      const int qb0 = (m * BM / kQuantBlockQ) * kQuantBlockQ;
+      const int qrows = min(kQuantBlockQ, Lq - qb0);
+      uint32_t mb = 0u;
+      for (int c = tid; c < kQuantBlockQ * (D / 8); c += C::kThreads) {
+        const int r = c / (D / 8), ch = 8 * (c % (D / 8));
+        if (r < qrows)
+          mb = absmax_bits(ld_global_16(a.Q + ((size_t)(q_row0 + qb0 + r) * a.Hq + hq) * D + ch), mb);
+      }
+      const float amax = wg_max(bits_max_float(mb));
+      const float d32 = amax / 127.0f;   // IEEE FP32 division
+      const float rcp = amax > 0.0f ? 1.0f / d32 : 0.0f;
+      dq = amax > 0.0f ? (float)(_Float16)d32 : 0.0f;
+      if (row_ok) {   // a zero block has rcp = 0: codes 0
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s) {
+          const uint4 c = codes16(ld_global_16(a.Q + qoff + 32 * s + 16 * hi),
+                                  ld_global_16(a.Q + qoff + 32 * s + 16 * hi + 8), d32, rcp);
+          q8f[s] = i32x4{(int)c.x, (int)c.y, (int)c.z, (int)c.w};
+        }
+      }
+    }
+  }
   const float c_fp16 = a.scale_log2e;
   const float c_int8_q = a.scale_log2e * dq;
-  if (need_int8) {   // key-block scales of the tiles this row visits (key block = key tile)
+  if (!OTF && need_int8) {   // key-block scales of the tiles this row visits (key block = key tile)
     for (int t = tid; t <= n_end; t += C::kThreads)
       key_scale[t] = a.dK[(size_t)(kblk0 + t) * a.Hk + hk];
   }
@@ -472,7 +562,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     route_ring = int8 ? (route_ring | bit) : (route_ring & ~bit);
     const uint32_t dst = smem_lds + (uint32_t)k_slot(iss_kt);
     const int rows = min(kBlockN, Lk - iss_kt * kBlockN);
-    if (int8)
+    if (int8 && !OTF)   // OTF stages every key tile in FP16
       dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(iss_k8, kstride / 2, rows, dst, wave, lane, plan_k8);
     else   // 8 copies per 64-channel half of the FP16 key tile
       dma_tile<C::kKRow, C::kKInstr, kBlockN, 8, 128>(iss_k, kstride, rows, dst, wave, lane, plan_k);
@@ -507,6 +597,42 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   const FragOffsets<128> fo_128(lane);      // K (FP16 halves), V^T, and K8 when d = 128
   const FragOffsets<C::kK8Row> fo_k8(lane);
 
+  // OTF: quantize the FP16 key tile in slot koff into the INT8 slot (K8 layout), with the
+  // blockwise rule of Appendix C over the tile's 64 keys; every thread of the workgroup takes
+  // part (two barriers).  Rows past L_k hold copies of the last key, so they leave the absmax
+  // unchanged.  Returns the FP16 bits of the tile's scale.
+  auto convert_k = [&](int koff) -> uint16_t {
+    constexpr int kGr = D / 16;                          // 16-code granules per key row
+    constexpr int kPer = kBlockN * kGr / C::kThreads;    // granules per thread
+    static_assert(kPer * C::kThreads == kBlockN * kGr, "granule split");
+    const char* src = smem + koff;
+    // FP16 granules 2*c8 and 2*c8 + 1 of 64-channel half c8 / 4 hold the 16 channels of
+    // INT8 granule c8.
+    auto fp16_off = [](int r, int c8, int j) {
+      const int c16 = (2 * c8 + j) & 7;
+      return ((2 * c8) >> 3) * C::kKHalfBytes + r * C::kKRow + 16 * (c16 ^ swz_key<128>(r));
+    };
+    uint32_t mb = 0u;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int gi = tid + i * C::kThreads, r = gi / kGr, c8 = gi % kGr;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) mb = absmax_bits(ld_lds_16(src, fp16_off(r, c8, j)), mb);
+    }
+    const float amax = wg_max(bits_max_float(mb));
+    const float d32 = amax / 127.0f;   // IEEE FP32 division
+    const float rcp = amax > 0.0f ? 1.0f / d32 : 0.0f;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {   // a zero block has rcp = 0: codes 0
+      const int gi = tid + i * C::kThreads, r = gi / kGr, c8 = gi % kGr;
+      *reinterpret_cast<uint4*>(smem + kK8Off + r * C::kK8Row + 16 * (c8 ^ swz_key<C::kK8Row>(r))) =
+          codes16(ld_lds_16(src, fp16_off(r, c8, 0)), ld_lds_16(src, fp16_off(r, c8, 1)), d32, rcp);
+    }
+    __syncthreads();   // codes visible to every wave; otf_red free again
+    const _Float16 sc = amax > 0.0f ? (_Float16)d32 : (_Float16)0.0f;   // RNE
+    return __builtin_bit_cast(uint16_t, sc);
+  };
+
   // Online-softmax state (Section 3.1), FP32; max kept in log2 units.
   float m_run = kNegInf;
   float msub = 0.0f;   // the max that P subtracts (0 while no score has been seen)
@@ -518,17 +644,18 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   // ---- Straight per-tile path, used for tiles that cross the causal diagonal or the sequence
   // end.  Raw scores of key tile n (INT32 products converted to float, or FP32 dot products)
   // and the factor c that turns them into log2-domain scaled scores.
-  auto qk = [&](int n, float (&sv)[32], float& c) {
+  // ks_otf: OTF only, the on-chip scale of tile n (its codes are in the INT8 slot).
+  auto qk = [&](int n, float (&sv)[32], float& c, uint16_t ks_otf) {
     const char* kst = smem + k_slot(n);
     if (route_of(n)) {
       i32x16 i0, i1;
-      qk_int8<D>(kst, fo_k8, q8f, i0, i1);
+      qk_int8<D>(OTF ? smem + kK8Off : kst, fo_k8, q8f, i0, i1);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         sv[r] = (float)i0[r];
         sv[16 + r] = (float)i1[r];
       }
-      c = c_int8_q * half_bits_to_float(key_scale[n]);
+      c = c_int8_q * half_bits_to_float(OTF ? ks_otf : key_scale[n]);
     } else {
       f32x16 f0, f1;
       qk_fp16<D>(kst, fo_128, qf, f0, f1);
@@ -697,25 +824,35 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   __syncthreads();
 
   f32x16 xa0, xa1, xb0, xb1;   // the two score buffers
+  uint16_t ks0 = 0;
+  if constexpr (OTF) {
+    if (n_split > 0 && route_of(0)) ks0 = convert_k(k_slot(0));
+  } else {
+    ks0 = key_scale[0];
+  }
   if (n_split > 0 && wave_active) {   // Q K^T of tile 0 and the running max it starts
     half8 unused_p[4];
     float unused_z;
     const bool int8 = route_of(0);
-    const bool fold = int8 && fold_ok(key_scale[0]);
-    if (fold) phase_a(QKInt8{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
-    else if (int8) phase_a(QKInt8Exact{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
+    const bool fold = int8 && fold_ok(ks0);
+    const int k8_off = OTF ? kK8Off : k_slot(0);
+    if (fold) phase_a(QKInt8{}, False{}, k8_off, xb0, xb1, xa0, xa1, unused_p, unused_z);
+    else if (int8) phase_a(QKInt8Exact{}, False{}, k8_off, xb0, xb1, xa0, xa1, unused_p, unused_z);
     else phase_a(QKFp16{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
-    set_tile(int8, fold, key_scale[0]);
+    set_tile(int8, fold, ks0);
     raise_max((pair_max(lane_max(xa0, xa1)) - bias_cur) * c_cur);
   }
   // Step n: scores of tile n in x, tile n + 1's go to y.
   auto step = [&](int n, const f32x16& x0, const f32x16& x1, f32x16& y0, f32x16& y1) {
     sync(n + 2, n + 1);   // K of tile n + 1 and V of tile n landed; K n + 2, V n + 1 in flight
-    if (!wave_active) return;
     const bool has_next = n + 1 < n_split;
     const bool int8 = has_next && route_of(n + 1);
-    const uint16_t ks = key_scale[min(n + 1, n_end)];
+    uint16_t ks;
+    if constexpr (OTF) ks = int8 ? convert_k(k_slot(n + 1)) : (uint16_t)0;   // whole workgroup
+    else ks = key_scale[min(n + 1, n_end)];
+    if (!wave_active) return;
     const bool fold = int8 && fold_ok(ks);
+    const int k8_off = OTF ? kK8Off : k_slot(n + 1);
     half8 pfr[4];
     float zs;
     if (!has_next) {
@@ -723,9 +860,9 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
       y1 = f32x16{};
       phase_a(QKNone{}, True{}, 0, x0, x1, y0, y1, pfr, zs);
     } else if (fold) {
-      phase_a(QKInt8{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
+      phase_a(QKInt8{}, True{}, k8_off, x0, x1, y0, y1, pfr, zs);
     } else if (int8) {
-      phase_a(QKInt8Exact{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
+      phase_a(QKInt8Exact{}, True{}, k8_off, x0, x1, y0, y1, pfr, zs);
     } else {
       phase_a(QKFp16{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
     }
@@ -751,9 +888,13 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   // waves whose rows see no key of a tile skip its math.
   for (n = n_split; n <= n_end; ++n) {
     sync(n + 1, n + 1);   // tile n landed; the slots of tile n - 1 take tile n + 1
+    uint16_t ks_otf = 0;
+    if constexpr (OTF) {
+      if (route_of(n)) ks_otf = convert_k(k_slot(n));   // whole workgroup
+    }
     if (wave_active && n * kBlockN <= wave_last_key) {
       float svm[32], c;
-      qk(n, svm, c);
+      qk(n, svm, c, ks_otf);
       half8 pfr[4];
       softmax_step<D, true>(svm, c, n * kBlockN, my_last_key, lane, m_run, z_run, oacc, pfr);
       pv(n, pfr);
@@ -827,12 +968,12 @@ __global__ __launch_bounds__(2 * BM) void debug_tiles_kernel(DebugTileArgs a) {
   }
 }
 
-template <int D, int BM, int HEADS>
+template <int D, int BM, int HEADS, bool OTF = false>
 hipError_t launch_attn_t(const AttnArgs& a, hipStream_t stream) {
   using C = TileCfg<D, BM, HEADS>;
   const long long grid = (long long)a.B * (a.Hq / HEADS) * a.T_m;
   if (grid <= 0 || grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS>), dim3((unsigned)grid),
+  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS, OTF>), dim3((unsigned)grid),
                      dim3(C::kThreads), 0, stream, a);
   return hipGetLastError();
 }
@@ -848,6 +989,14 @@ hipError_t launch_debug_t(const DebugTileArgs& a, hipStream_t stream) {
 
 hipError_t launch_routed_attention(const AttnArgs& a, int d, int block_m, hipStream_t stream) {
   // One query head per workgroup; two workgroups share a CU.
+  if (a.on_the_fly) {
+    if (a.seqs) return hipErrorInvalidValue;
+    if (d == 128 && block_m == 128) return launch_attn_t<128, 128, 1, true>(a, stream);
+    if (d == 128 && block_m == 64) return launch_attn_t<128, 64, 1, true>(a, stream);
+    if (d == 64 && block_m == 128) return launch_attn_t<64, 128, 1, true>(a, stream);
+    if (d == 64 && block_m == 64) return launch_attn_t<64, 64, 1, true>(a, stream);
+    return hipErrorInvalidValue;
+  }
   if (d == 128 && block_m == 128) return launch_attn_t<128, 128, TM_HEADS>(a, stream);
   if (d == 128 && block_m == 64) return launch_attn_t<128, 64, 1>(a, stream);
   if (d == 64 && block_m == 128) return launch_attn_t<64, 128, 1>(a, stream);

@@ -93,7 +93,9 @@ struct Plan {
   size_t seq_off, q8_off, k8_off, dq_off, dk_off, vt_off, total;
 };
 
-Plan make_plan(const tilemix_params* p, long long total_q = -1, long long total_k = -1) {
+// fused: the on-the-fly operand mode, whose workspace holds the V tiles only.
+Plan make_plan(const tilemix_params* p, long long total_q = -1, long long total_k = -1,
+               bool fused = false) {
   Plan pl{};
   pl.T_m = cdiv(p->len_q, p->block_m);
   pl.T_n = cdiv(p->len_k, p->block_n);
@@ -109,10 +111,10 @@ Plan make_plan(const tilemix_params* p, long long total_q = -1, long long total_
   const long long kblocks = varlen ? cdiv(total_k, tilemix::kQuantBlockK) + p->batch : p->batch * pl.nKB;
   const long long ktiles = varlen ? cdiv(total_k, tilemix::kBlockN) + p->batch : p->batch * pl.T_n;
   pl.seq_bytes = varlen ? (size_t)(p->batch + 1) * tilemix::kSeqFields * sizeof(int) : 0;
-  pl.q8_bytes = (size_t)rows_q * p->heads_q * d;
-  pl.k8_bytes = (size_t)rows_k * p->heads_kv * d;
-  pl.dq_bytes = (size_t)qblocks * p->heads_q * 2;
-  pl.dk_bytes = (size_t)kblocks * p->heads_kv * 2;
+  pl.q8_bytes = fused ? 0 : (size_t)rows_q * p->heads_q * d;
+  pl.k8_bytes = fused ? 0 : (size_t)rows_k * p->heads_kv * d;
+  pl.dq_bytes = fused ? 0 : (size_t)qblocks * p->heads_q * 2;
+  pl.dk_bytes = fused ? 0 : (size_t)kblocks * p->heads_kv * 2;
   pl.vt_bytes = (size_t)ktiles * p->heads_kv * d * tilemix::kBlockN * 2;
   pl.seq_off = 0;
   pl.q8_off = align256(pl.seq_off + pl.seq_bytes);
@@ -159,9 +161,10 @@ tilemix_status check_workspace(const Plan& pl, const void* workspace, size_t wor
 }
 
 // seqs: the sequence table of a variable-length batch (in the workspace), or nullptr.
+// fused: the on-the-fly operand mode (no quantize-once pass).
 tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void* Q, const void* K,
                             const void* V, void* workspace, hipStream_t s,
-                            const int* seqs = nullptr) {
+                            const int* seqs = nullptr, bool fused = false) {
   char* ws = static_cast<char*>(workspace);
   int8_t* q8 = reinterpret_cast<int8_t*>(ws + pl.q8_off);
   int8_t* k8 = reinterpret_cast<int8_t*>(ws + pl.k8_off);
@@ -169,7 +172,7 @@ tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void*
   uint16_t* dk = reinterpret_cast<uint16_t*>(ws + pl.dk_off);
   _Float16* vt = reinterpret_cast<_Float16*>(ws + pl.vt_off);
   tilemix_status st;
-  if (p.route_hint != 0) {   // an all-FP16 map skips the quantize-once pass
+  if (p.route_hint != 0 && !fused) {   // an all-FP16 map skips the quantize-once pass
     st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(Q), q8, dq, p.batch,
                                              p.len_q, p.heads_q, p.head_dim,
                                              tilemix::kQuantBlockQ, seqs, false, s), "quantize Q");
@@ -185,7 +188,7 @@ tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void*
 
 tilemix_status attend_impl(const tilemix_params& p, const Plan& pl, const void* Q, const void* K,
                            const uint64_t* route_bits, void* O, const void* workspace,
-                           hipStream_t s, const int* seqs = nullptr) {
+                           hipStream_t s, const int* seqs = nullptr, bool fused = false) {
   const char* ws = static_cast<const char*>(workspace);
   tilemix::AttnArgs a{};
   a.seqs = seqs;
@@ -203,6 +206,7 @@ tilemix_status attend_impl(const tilemix_params& p, const Plan& pl, const void* 
   a.nQB = (int)pl.nQB; a.nKB = (int)pl.nKB;
   a.causal = p.causal;
   a.force_fp16 = p.route_hint == 0 ? 1 : 0;
+  a.on_the_fly = fused ? 1 : 0;
   a.route_batch_stride = p.route_per_batch ? (long long)p.heads_kv * pl.T_m * pl.W : 0;
   a.scale_log2e = p.scale * 1.4426950408889634f;
   return hip_status(tilemix::launch_routed_attention(a, p.head_dim, p.block_m, s), "routed attention");
@@ -236,6 +240,30 @@ tilemix_status tilemix_prefill(const tilemix_params* params, const void* Q, cons
   hipStream_t s = static_cast<hipStream_t>(stream);
   if ((st = prepare_impl(*params, pl, Q, K, V, workspace, s)) != TILEMIX_OK) return st;
   if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, s)) != TILEMIX_OK) return st;
+  return ok();
+}
+
+tilemix_status tilemix_fused_workspace_size(const tilemix_params* params, size_t* bytes) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  if (!bytes) return fail(TILEMIX_ERR_NULL, "bytes is NULL");
+  *bytes = make_plan(params, -1, -1, true).total;
+  return ok();
+}
+
+tilemix_status tilemix_prefill_fused(const tilemix_params* params, const void* Q, const void* K,
+                                     const void* V, const uint64_t* route_bits, void* O,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
+  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
+  const Plan pl = make_plan(params, -1, -1, true);
+  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = prepare_impl(*params, pl, Q, K, V, workspace, s, nullptr, true)) != TILEMIX_OK) return st;
+  if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, s, nullptr, true)) != TILEMIX_OK)
+    return st;
   return ok();
 }
 

@@ -55,10 +55,17 @@ __device__ __forceinline__ float pair_sum(float x) {
 // vector load; it is issued as inline assembly so that the only waits on it are the explicit
 // vmcnt waits of the caller (the compiler would otherwise wait for every copy in flight
 // before any LDS read, whichever LDS bytes the copies write).
+// base and lds_addr pass through readfirstlane (a no-op on values the compiler already holds in
+// scalar registers), so that the scalar operands stay scalar where its uniformity analysis
+// loses track of them.
 __device__ __forceinline__ void dma_16(const void* base, uint32_t voff, uint32_t lds_addr) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  const uint64_t bs = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+  const uint32_t ls = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_addr);
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                :
-               : "v"(voff), "s"(base), "s"(lds_addr)
+               : "v"(voff), "s"((const void*)(uintptr_t)bs), "s"(ls)
                : "m0");
 }
 

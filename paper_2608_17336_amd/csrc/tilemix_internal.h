@@ -47,6 +47,7 @@ struct AttnArgs {
   int nQB, nKB;
   int causal;
   int force_fp16;         // 1: ignore routing words, every tile takes the FP16 path
+  int on_the_fly;         // 1: no Q8/K8/scales; the kernel quantizes Q and INT8 key tiles on chip
   long long route_batch_stride;  // words between the maps of consecutive sequences (0 = shared)
   float scale_log2e;      // softmax scale * log2(e)
 };
