@@ -989,7 +989,9 @@ hipError_t launch_debug_t(const DebugTileArgs& a, hipStream_t stream) {
 
 hipError_t launch_routed_attention(const AttnArgs& a, int d, int block_m, hipStream_t stream) {
   // One query head per workgroup; two workgroups share a CU.
-  if (a.on_the_fly) {
+  // On-the-fly operands: an all-FP16 map has nothing to quantize, and the quantize-once kernel
+  // then reads neither Q8 nor K8 nor their scales.
+  if (a.on_the_fly && !a.force_fp16) {
     if (a.seqs) return hipErrorInvalidValue;
     if (d == 128 && block_m == 128) return launch_attn_t<128, 128, 1, true>(a, stream);
     if (d == 128 && block_m == 64) return launch_attn_t<128, 64, 1, true>(a, stream);
