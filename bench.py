@@ -103,7 +103,7 @@ def cpu_baseline(cfg, Q, K, V, words, budget_rows=None):
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"{idx.size} query rows (every {stride}th) of head 0 of {cfg.name}, "
+        "sample": (f"{idx.size} query rows (one in {stride}) of head 0 of {cfg.name}, "
                    f"{pairs} legal pairs incl. the oracle's own quantization of that head, "
                    f"{dt:.1f} s; full pass extrapolates to {full / 3600:.1f} h"),
         "seconds": dt,
