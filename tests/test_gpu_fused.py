@@ -108,6 +108,24 @@ def test_fused_unequal_lengths_bitwise():
         assert same_bits(O1, O2), causal
 
 
+def test_fused_longest_key_sequence_bitwise():
+    """L_k = 262144 with g = 1 (64 routing words per row), L_q = 200: fused equals quantize-once."""
+    import paper_2608_17336_amd as tm
+    import torch
+    rng = np.random.default_rng(262145)
+    Lq, Lk, d = 200, 262144, 128
+    q = to_dev(rng.standard_normal((1, Lq, 2, d)).astype(np.float16))
+    k = to_dev(rng.standard_normal((1, Lk, 1, d)).astype(np.float16))
+    v = to_dev(rng.standard_normal((1, Lk, 1, d)).astype(np.float16))
+    words = rng.integers(0, 2 ** 63, size=(1, 1, 2, 64), dtype=np.int64)
+    w = to_dev(words)
+    for causal in (True, False):
+        O1 = tm.tilemix_prefill(q, k, v, w, 1, (128, 64), causal, 1 / np.sqrt(d))
+        O2 = tm.tilemix_prefill_fused(q, k, v, w, 1, (128, 64), causal, 1 / np.sqrt(d))
+        torch.cuda.synchronize()
+        assert same_bits(O1, O2), causal
+
+
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("name", ["8k-gqa", "32k-gqa"])
 def test_fused_full_workload_bitwise(name):

@@ -139,6 +139,39 @@ def test_unequal_lengths_bottom_right_causal():
         assert mx <= MAX_ABS and rel <= REL_L2
 
 
+@pytest.mark.timeout(600)
+def test_longest_key_sequence_64_routing_words():
+    """L_k = 262144, the longest key sequence the build takes: with g = 1 a routing row is 64
+    words, the most the kernel holds (one per lane).  A ragged L_q = 200 query block at the end
+    of the sequence (bottom-right causal) and the non-causal case, against the oracle on
+    sampled rows."""
+    import paper_2608_17336_amd as tm
+    import torch
+    rng = np.random.default_rng(262144)
+    Lq, Lk, d = 200, 262144, 128
+    Q = rng.standard_normal((1, Lq, 2, d)).astype(np.float16)
+    K = rng.standard_normal((1, Lk, 1, d)).astype(np.float16)
+    V = rng.standard_normal((1, Lk, 1, d)).astype(np.float16)
+    T_m, T_n = -(-Lq // 128), -(-Lk // 64)
+    R = (rng.random((1, T_m, T_n)) < 0.5).astype(np.uint8)
+    words = pack_route_bits(R)
+    assert words.shape[-1] == 64
+    q, k, v, w = to_dev(Q), to_dev(K), to_dev(V), to_dev(words)
+    idx = np.unique(np.concatenate([np.arange(8), np.arange(Lq - 8, Lq), [127, 128],
+                                    rng.choice(Lq, 16, replace=False)]))
+    rows = [(0, h, idx) for h in range(2)]
+    ops = OracleOperands.from_inputs(Q, K, q_heads=[(0, 0), (0, 1)], k_heads=[(0, 0)])
+    for causal in (True, False):
+        log(f"Lq={Lq} Lk={Lk} causal={causal}")
+        O = tm.tilemix_prefill(q, k, v, w, 1, (128, 64), causal, 1 / math.sqrt(d))
+        torch.cuda.synchronize()
+        ref = routed_attention_rows(Q, K, V, words, block_m=128, block_n=64, group_size=1,
+                                    causal=causal, scale=1 / math.sqrt(d), rows=rows, operands=ops)
+        mx, rel = compare_rows(O, rows, ref)
+        log(f"  max_abs={mx:.3e} rel_l2={rel:.3e}")
+        assert mx <= MAX_ABS and rel <= REL_L2, (causal, mx, rel)
+
+
 # --------------------------------------------------------------------- full-size workloads
 
 WL = [(name, mi) for name, cfg in WORKLOADS.items() for mi in range(len(cfg.masks))]
