@@ -108,6 +108,24 @@ def test_fused_unequal_lengths_bitwise():
         assert same_bits(O1, O2), causal
 
 
+def test_fused_per_sequence_routes_bitwise():
+    """route_per_batch: each sequence reads its own routing map (B_r = B)."""
+    import paper_2608_17336_amd as tm
+    import torch
+    cfg = small_workload("rpb", B=3, Hq=4, Hk=2, d=128, L=700, block_m=128, group_size=2, index=671)
+    Q, K, V = make_qkv(cfg)
+    q, k, v = to_dev(Q), to_dev(K), to_dev(V)
+    p = tm.Params(cfg.B, cfg.Hq, cfg.Hk, cfg.L, cfg.L, cfg.d, cfg.block_m, cfg.block_n, cfg.group_size)
+    W = tm.tilemix_route_words_per_row(p)
+    words = np.random.default_rng(671).integers(0, 2 ** 63, size=(cfg.B, cfg.Hk, p.T_m, W), dtype=np.int64)
+    w = to_dev(words)
+    O1 = tm.tilemix_prefill(q, k, v, w, cfg.group_size, (128, 64), True, cfg.scale, route_per_batch=True)
+    O2 = tm.tilemix_prefill_fused(q, k, v, w, cfg.group_size, (128, 64), True, cfg.scale,
+                                  route_per_batch=True)
+    torch.cuda.synchronize()
+    assert same_bits(O1, O2)
+
+
 def test_fused_longest_key_sequence_bitwise():
     """L_k = 262144 with g = 1 (64 routing words per row), L_q = 200: fused equals quantize-once."""
     import paper_2608_17336_amd as tm
