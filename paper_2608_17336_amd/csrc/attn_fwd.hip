@@ -721,6 +721,10 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     float c_x = c_cur, k_x = k_cur;
     asm volatile("" : "+v"(c_x), "+v"(k_x));
     float zs0 = 0.0f, zs1 = 0.0f;
+    // Wave priorities (the SIMD's other wave belongs to the other workgroup on this CU): the
+    // phase that mixes matrix-core and vector work issues first, the pure P.V phase next, and
+    // the barrier and copy code last.
+    __builtin_amdgcn_s_setprio(2);
     static_for<0, NQ>([&](auto jc) {
       constexpr int j = decltype(jc)::value;
       if constexpr (kQK != 0) {
@@ -750,6 +754,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
       }
       __builtin_amdgcn_sched_barrier(0);
     });
+    __builtin_amdgcn_s_setprio(0);
     zs = zs0 + zs1;
   };
 
@@ -763,6 +768,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
       vf[j] = ld_lds_16(vst, fo_128.at(t) + cc * 32 * C::kVRow);
     };
     static_for<0, (kLeadB < NP ? kLeadB : NP)>(vload);
+    __builtin_amdgcn_s_setprio(1);
     static_for<0, NP>([&](auto jc) {
       constexpr int j = decltype(jc)::value;
       if constexpr (j + kLeadB < NP) vload(std::integral_constant<int, j + kLeadB>{});
@@ -770,6 +776,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
       oacc[cc] = mfma_f16(as_half8(vf[j]), pfr[t], oacc[cc]);
       __builtin_amdgcn_sched_barrier(0);
     });
+    __builtin_amdgcn_s_setprio(0);
   };
 
   // Lane max of a tile's 32 raw scores.
