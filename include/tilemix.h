@@ -85,8 +85,10 @@ typedef struct tilemix_params {
 /* Words per routing row, W = ceil(ceil(ceil(L_k / BLOCK_N) / g) / 64); 0 if params invalid. */
 int32_t tilemix_route_words_per_row(const tilemix_params* params);
 
-/* Bytes of device workspace tilemix_prefill needs (Q8, K8, their FP16 block scales and
- * V laid out per 64-key tile); the workspace must be 256-byte aligned. */
+/* Bytes of device workspace tilemix_prefill needs (K8, its FP16 block scales and V laid out
+ * per 64-key tile); the workspace must be 256-byte aligned.  No Q8 tensor is kept: a 128-row
+ * query block belongs to one workgroup of the attention kernel (two when BLOCK_M is 64), which
+ * quantizes it in its prologue with the same codes and scale as tilemix_quantize. */
 tilemix_status tilemix_workspace_size(const tilemix_params* params, size_t* bytes);
 
 /*
@@ -108,14 +110,14 @@ tilemix_status tilemix_prefill(const tilemix_params* params,
 /*
  * tilemix_prefill_fused -- tilemix_prefill in the fused on-the-fly operand mode (Appendix D,
  * "Storage and Execution Layout", the fused on-the-fly mode; Appendix C quantization rules):
- * no Q8 / K8 / scale tensors and no quantization pass.  The kernel computes the scales and
- * codes on chip, only for what INT8-routed groups use: each workgroup quantizes the 128-row
- * query block of its rows once, and every INT8-routed 64-key tile (one key scale block) after
- * its FP16 copy reaches LDS.  Codes and scales equal those of tilemix_quantize, so the output
+ * no K8 / scale tensors and no quantization pass.  The kernel computes the scales and codes
+ * on chip, only for what INT8-routed groups use: each workgroup quantizes the 128-row query
+ * block of its rows once (as tilemix_prefill does too), and every INT8-routed 64-key tile (one
+ * key scale block) after its FP16 copy reaches LDS.  Codes and scales equal those of tilemix_quantize, so the output
  * equals tilemix_prefill's bit for bit.  Arguments as in tilemix_prefill; the workspace
  * (tilemix_fused_workspace_size bytes) holds only V laid out per 64-key tile.  The INT8 route
  * costs more per tile here (every workgroup requantizes the key tiles it reads); the mode
- * trades that time for the Q8 / K8 scratch.
+ * trades that time for the K8 scratch.
  */
 tilemix_status tilemix_fused_workspace_size(const tilemix_params* params, size_t* bytes);
 
@@ -125,11 +127,11 @@ tilemix_status tilemix_prefill_fused(const tilemix_params* params,
                                      void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * tilemix_prepare -- the first half of tilemix_prefill: the quantize-once pass (Q8, K8 and
- * their FP16 block scales, Appendix C "Quantize-Once Execution"; skipped when route_hint is 0)
- * and the per-64-key-tile V layout, written into `workspace`.  Arguments as in
- * tilemix_prefill.  The workspace then serves any number of tilemix_attend calls on the same
- * Q, K and V.
+ * tilemix_prepare -- the first half of tilemix_prefill: the quantize-once pass over the keys
+ * (K8 and its FP16 block scales, Appendix C "Quantize-Once Execution"; skipped when route_hint
+ * is 0) and the per-64-key-tile V layout, written into `workspace`.  The query blocks are
+ * quantized by tilemix_attend itself, once per block.  Arguments as in tilemix_prefill (Q is
+ * not read).  The workspace then serves any number of tilemix_attend calls on the same K and V.
  */
 tilemix_status tilemix_prepare(const tilemix_params* params, const void* Q, const void* K,
                                const void* V, void* workspace, size_t workspace_bytes,

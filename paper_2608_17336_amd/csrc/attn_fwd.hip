@@ -8,9 +8,11 @@
 //      workgroup, so one branch selects which K form (FP16 K or INT8 K8) is staged;
 //   2. computes the transposed score tile S^T (keys x queries) on the matrix cores:
 //        FP16 route: v_mfma_f32_32x32x16_f16, K from LDS x Q from registers;
-//        INT8 route: v_mfma_i32_32x32x32_i8 on the quantize-once codes, exact INT32,
-//                    then one FP32 factor scale*log2(e)*dQ*dK (Appendix C rescale),
-//                    applied in the exp argument;
+//        INT8 route: v_mfma_i32_32x32x32_i8 on the INT8 codes, exact INT32, then one
+//                    FP32 factor scale*log2(e)*dQ*dK (Appendix C rescale), applied in the
+//                    exp argument.  The key codes come from the quantize-once pass; the
+//                    query codes are made in the workgroup's prologue, since a 128-row query
+//                    block belongs to one workgroup (two for BLOCK_M = 64);
 //      with keys on the matrix rows, every lane holds all scores of one query row for
 //      16 keys of each 32-key block, so row max / row sum are in-lane plus one exchange
 //      between the two half-waves;
@@ -40,9 +42,6 @@
 #include "tilemix_device.h"
 #include "tilemix_internal.h"
 
-#ifndef TM_HEADS
-#define TM_HEADS 1
-#endif
 
 namespace tilemix {
 
@@ -302,13 +301,6 @@ __device__ __forceinline__ void decode_unit(int id, int B, int Hq, int Hk, int T
   hq0 = hk * (Hq / Hk) + qg * HEADS;
 }
 
-__device__ __forceinline__ float load_scale_uniform(const uint16_t* base, size_t idx) {
-  // The scale arrays live in 256-byte aligned workspace slots, so reading the aligned
-  // 32-bit word that holds element idx stays inside the slot.
-  const uint32_t w = reinterpret_cast<const uint32_t*>(base)[idx >> 1];
-  return half_bits_to_float((uint16_t)((idx & 1) ? (w >> 16) : (w & 0xffffu)));
-}
-
 // max(a, b, c) in one instruction.  The scores are never NaN, so the operand quieting that a
 // library max would add is not needed.
 __device__ __forceinline__ float max3f(float a, float b, float c) {
@@ -351,7 +343,7 @@ __device__ __forceinline__ void exp_pair(const f32x16& x0, const f32x16& x1, flo
 template <int D, int BM, int HEADS, bool OTF = false>
 __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) {
   using C = TileCfg<D, BM, HEADS>;
-  static_assert(!OTF || HEADS == 1, "on-the-fly operands: one query head per workgroup");
+  static_assert(HEADS == 1, "the query-block quantization reduces over the whole workgroup");
   // Two K slots and two V slots: step n reads K of tile n + 1 and V of tile n while K of tile
   // n + 2 and V of tile n + 1 are copied into the slots that step n - 1 released.  72 KB at
   // d = 128, so two workgroups share a CU and each SIMD runs one wave of each.
@@ -367,7 +359,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   // of this routing row and of this KV head's first V tile.
   int Lq = a.Lq, Lk = a.Lk;
   long long q_row0 = (long long)b * a.Lq, k_row0 = (long long)b * a.Lk;
-  long long qblk0 = (long long)b * a.nQB, kblk0 = (long long)b * a.nKB;
+  long long kblk0 = (long long)b * a.nKB;
   const uint64_t* route_row =
       a.route + (size_t)b * a.route_batch_stride + ((size_t)hk * a.T_m + m) * a.W;
   long long vt_tile0 = ((long long)b * a.Hk + hk) * a.T_n;
@@ -378,7 +370,6 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     if (m * BM >= Lq) return;   // past the end of a shorter sequence: no rows to write
     q_row0 = e[kSeqQStart];
     k_row0 = e[kSeqKStart];
-    qblk0 = e[kSeqQBlk];
     kblk0 = e[kSeqKBlk];
     route_row = a.route + ((size_t)(e[kSeqQTile] + m) * a.Hk + hk) * a.W;
     vt_tile0 = (long long)hk * a.seqs[kSeqFields * a.B + kSeqKTile] + e[kSeqKTile];
@@ -443,11 +434,8 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     qf[s] = (need_fp16 && row_ok) ? as_half8(ld_global_16(a.Q + qoff + 16 * s + 8 * hi)) : half8{};
 #pragma unroll
   for (int s = 0; s < D / 32; ++s)
-    q8f[s] = (!OTF && need_int8 && row_ok) ? as_i32x4(ld_global_16(a.Q8 + qoff + 32 * s + 16 * hi))
-                                           : i32x4{};
-  float dq = (!OTF && need_int8 && wave_active)
-                 ? load_scale_uniform(a.dQ, (size_t)(qblk0 + q0 / kQuantBlockQ) * a.Hq + hq)
-                 : 0.0f;
+    q8f[s] = i32x4{};
+  float dq = 0.0f;   // the FP16-stored scale of this row's query block (set below)
 
   // OTF: maximum of a per-thread value over the workgroup (every thread gets it).
   auto wg_max = [&](float v) {
@@ -503,7 +491,11 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     return make_uint4(pack4(w[0], w[1], w[2], w[3]), pack4(w[4], w[5], w[6], w[7]),
                       pack4(w[8], w[9], w[10], w[11]), pack4(w[12], w[13], w[14], w[15]));
   };
-  if constexpr (OTF) {
+  // The query operands of the INT8 route are made here, in both operand modes: the 128-row
+  // query block of this row (Appendix C) is this workgroup's own rows (BLOCK_M = 128) or those of
+  // two workgroups (64), so each block is quantized once, with the codes and scale of the
+  // quantize-once rule, and no Q8 tensor passes through HBM.
+  {
     if (need_int8) {   // the same for every wave of the workgroup
       // Q block of this row: rows qb0 .. qb0 + 127 of the sequence (those that exist).
       const int qb0 = (m * BM / kQuantBlockQ) * kQuantBlockQ;
@@ -1006,7 +998,7 @@ hipError_t launch_routed_attention(const AttnArgs& a, int d, int block_m, hipStr
     if (d == 64 && block_m == 64) return launch_attn_t<64, 64, 1, true>(a, stream);
     return hipErrorInvalidValue;
   }
-  if (d == 128 && block_m == 128) return launch_attn_t<128, 128, TM_HEADS>(a, stream);
+  if (d == 128 && block_m == 128) return launch_attn_t<128, 128, 1>(a, stream);
   if (d == 128 && block_m == 64) return launch_attn_t<128, 64, 1>(a, stream);
   if (d == 64 && block_m == 128) return launch_attn_t<64, 128, 1>(a, stream);
   if (d == 64 && block_m == 64) return launch_attn_t<64, 64, 1>(a, stream);

@@ -88,9 +88,9 @@ long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 // blocks or tiles, and its workspace starts with the device-built sequence table.
 struct Plan {
   long long T_m, T_n, T_mask, W;
-  long long nQB, nKB;
-  size_t seq_bytes, q8_bytes, k8_bytes, dq_bytes, dk_bytes, vt_bytes;
-  size_t seq_off, q8_off, k8_off, dq_off, dk_off, vt_off, total;
+  long long nKB;
+  size_t seq_bytes, k8_bytes, dk_bytes, vt_bytes;
+  size_t seq_off, k8_off, dk_off, vt_off, total;
 };
 
 // fused: the on-the-fly operand mode, whose workspace holds the V tiles only.
@@ -101,26 +101,21 @@ Plan make_plan(const tilemix_params* p, long long total_q = -1, long long total_
   pl.T_n = cdiv(p->len_k, p->block_n);
   pl.T_mask = cdiv(pl.T_n, p->group_size);
   pl.W = cdiv(pl.T_mask, 64);
-  pl.nQB = cdiv(p->len_q, tilemix::kQuantBlockQ);
   pl.nKB = cdiv(p->len_k, tilemix::kQuantBlockK);
   const size_t d = (size_t)p->head_dim;
   const bool varlen = total_q >= 0;
-  const long long rows_q = varlen ? total_q : (long long)p->batch * p->len_q;
   const long long rows_k = varlen ? total_k : (long long)p->batch * p->len_k;
-  const long long qblocks = varlen ? cdiv(total_q, tilemix::kQuantBlockQ) + p->batch : p->batch * pl.nQB;
   const long long kblocks = varlen ? cdiv(total_k, tilemix::kQuantBlockK) + p->batch : p->batch * pl.nKB;
   const long long ktiles = varlen ? cdiv(total_k, tilemix::kBlockN) + p->batch : p->batch * pl.T_n;
   pl.seq_bytes = varlen ? (size_t)(p->batch + 1) * tilemix::kSeqFields * sizeof(int) : 0;
-  pl.q8_bytes = fused ? 0 : (size_t)rows_q * p->heads_q * d;
+  // The attention kernel quantizes each query block itself (one workgroup per block), so only
+  // the key operands of the quantize-once pass live in the workspace.
   pl.k8_bytes = fused ? 0 : (size_t)rows_k * p->heads_kv * d;
-  pl.dq_bytes = fused ? 0 : (size_t)qblocks * p->heads_q * 2;
   pl.dk_bytes = fused ? 0 : (size_t)kblocks * p->heads_kv * 2;
   pl.vt_bytes = (size_t)ktiles * p->heads_kv * d * tilemix::kBlockN * 2;
   pl.seq_off = 0;
-  pl.q8_off = align256(pl.seq_off + pl.seq_bytes);
-  pl.k8_off = align256(pl.q8_off + pl.q8_bytes);
-  pl.dq_off = align256(pl.k8_off + pl.k8_bytes);
-  pl.dk_off = align256(pl.dq_off + pl.dq_bytes);
+  pl.k8_off = align256(pl.seq_off + pl.seq_bytes);
+  pl.dk_off = align256(pl.k8_off + pl.k8_bytes);
   pl.vt_off = align256(pl.dk_off + pl.dk_bytes);
   pl.total = align256(pl.vt_off + pl.vt_bytes);
   return pl;
@@ -162,21 +157,16 @@ tilemix_status check_workspace(const Plan& pl, const void* workspace, size_t wor
 
 // seqs: the sequence table of a variable-length batch (in the workspace), or nullptr.
 // fused: the on-the-fly operand mode (no quantize-once pass).
-tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void* Q, const void* K,
+// Q is not read here: the attention kernel quantizes the query blocks itself.
+tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void* /*Q*/, const void* K,
                             const void* V, void* workspace, hipStream_t s,
                             const int* seqs = nullptr, bool fused = false) {
   char* ws = static_cast<char*>(workspace);
-  int8_t* q8 = reinterpret_cast<int8_t*>(ws + pl.q8_off);
   int8_t* k8 = reinterpret_cast<int8_t*>(ws + pl.k8_off);
-  uint16_t* dq = reinterpret_cast<uint16_t*>(ws + pl.dq_off);
   uint16_t* dk = reinterpret_cast<uint16_t*>(ws + pl.dk_off);
   _Float16* vt = reinterpret_cast<_Float16*>(ws + pl.vt_off);
   tilemix_status st;
   if (p.route_hint != 0 && !fused) {   // an all-FP16 map skips the quantize-once pass
-    st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(Q), q8, dq, p.batch,
-                                             p.len_q, p.heads_q, p.head_dim,
-                                             tilemix::kQuantBlockQ, seqs, false, s), "quantize Q");
-    if (st != TILEMIX_OK) return st;
     st = hip_status(tilemix::launch_quantize(static_cast<const _Float16*>(K), k8, dk, p.batch,
                                              p.len_k, p.heads_kv, p.head_dim,
                                              tilemix::kQuantBlockK, seqs, true, s), "quantize K");
@@ -195,15 +185,13 @@ tilemix_status attend_impl(const tilemix_params& p, const Plan& pl, const void* 
   a.Q = static_cast<const _Float16*>(Q);
   a.K = static_cast<const _Float16*>(K);
   a.Vt = reinterpret_cast<const _Float16*>(ws + pl.vt_off);
-  a.Q8 = reinterpret_cast<const int8_t*>(ws + pl.q8_off);
   a.K8 = reinterpret_cast<const int8_t*>(ws + pl.k8_off);
-  a.dQ = reinterpret_cast<const uint16_t*>(ws + pl.dq_off);
   a.dK = reinterpret_cast<const uint16_t*>(ws + pl.dk_off);
   a.route = route_bits;
   a.O = static_cast<_Float16*>(O);
   a.B = p.batch; a.Hq = p.heads_q; a.Hk = p.heads_kv; a.Lq = p.len_q; a.Lk = p.len_k;
   a.T_m = (int)pl.T_m; a.T_n = (int)pl.T_n; a.W = (int)pl.W; a.g = p.group_size;
-  a.nQB = (int)pl.nQB; a.nKB = (int)pl.nKB;
+  a.nKB = (int)pl.nKB;
   a.causal = p.causal;
   a.force_fp16 = p.route_hint == 0 ? 1 : 0;
   a.on_the_fly = fused ? 1 : 0;

@@ -31,23 +31,21 @@ struct AttnArgs {
   const _Float16* Q;      // [B, Lq, Hq, d]
   const _Float16* K;      // [B, Lk, Hk, d]
   const _Float16* Vt;     // [B, Hk, T_n, d, 64]: V per 64-key tile, d-major, keys permuted
-  const int8_t* Q8;       // [B, Lq, Hq, d]
   const int8_t* K8;       // [B, Lk, Hk, d]
-  const uint16_t* dQ;     // FP16 bits [B, nQB, Hq]
   const uint16_t* dK;     // FP16 bits [B, nKB, Hk]
   const uint64_t* route;  // [B_r, Hk, T_m, W]
   _Float16* O;            // [B, Lq, Hq, d]
   // Variable-length batch: sequence table (see kSeqFields), or nullptr when every sequence has
-  // the lengths Lq / Lk.  With a table, Lq / Lk are the maximum lengths, Q/K/V/O/Q8/K8 are
+  // the lengths Lq / Lk.  With a table, Lq / Lk are the maximum lengths, Q/K/V/O/K8 are
   // packed [rows, H, d], scales [blocks, H], V tiles [Hk, key tiles, d, 64] and routing rows
   // [query-tile rows, Hk, W].
   const int* seqs;
   int B, Hq, Hk, Lq, Lk;
   int T_m, T_n, W, g;
-  int nQB, nKB;
+  int nKB;
   int causal;
   int force_fp16;         // 1: ignore routing words, every tile takes the FP16 path
-  int on_the_fly;         // 1: no Q8/K8/scales; the kernel quantizes Q and INT8 key tiles on chip
+  int on_the_fly;         // 1: no K8/scales either; the kernel quantizes INT8 key tiles on chip
   long long route_batch_stride;  // words between the maps of consecutive sequences (0 = shared)
   float scale_log2e;      // softmax scale * log2(e)
 };
