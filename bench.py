@@ -439,6 +439,13 @@ def bench_varlen(args, cfg, mask):
                    "mask": mask.label, "rho_pairs": round(rho, 4)},
         "step_ms_events": round(ms, 4),
         "pct_of_weighted_roofline": round(100.0 * t_star / (wall * 1e-3), 2),
+        # one call enqueues the sequence table, the key quantization, the V tiles and the kernel,
+        # so the achieved rate is over the whole event-timed call
+        "roofline": {"bound": "mfma", "achieved": round(flops / (ms * 1e-3) / 1e12, 2),
+                     "peak": round(flops / t_star / 1e12, 2), "unit": "TFLOP/s",
+                     "frac": round(t_star / (ms * 1e-3), 4), "traffic": None,
+                     "kernel": f"tilemix_prefill_varlen (seq table, K quantization, V tiles, "
+                               f"routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1>)"},
     }
     print(json.dumps(line), flush=True)
     return 0
