@@ -50,17 +50,18 @@ def flop_model(cfg, rho_pairs):
             "t_star_s": t_star, "weighted_peak": total / t_star}
 
 
-def kernel_source_digest():
-    """SHA-256 of the attention kernel's source: HBM traffic counters belong to one build."""
-    path = os.path.join(ROOT, "paper_2608_17336_amd", "csrc", "attn_fwd.hip")
+def kernel_source_digest(source="attn_fwd.hip"):
+    """SHA-256 of a kernel source file: HBM traffic counters belong to one build."""
+    path = os.path.join(ROOT, "paper_2608_17336_amd", "csrc", source)
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def recorded_traffic(workload):
-    """HBM bytes per attention launch from the committed counter summary of this workload,
-    or None when there is none or it was taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", f"routed_attn_fwd_{workload}_hbm_traffic.md")
+def recorded_traffic(profile, mask_label, source="attn_fwd.hip"):
+    """HBM bytes per launch (per step for decode) from the committed counter summary
+    profiles/<profile>_hbm_traffic.md, or None when there is none, or it was taken with another
+    routing mask or on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{profile}_hbm_traffic.md")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -69,12 +70,26 @@ def recorded_traffic(workload):
             m = re.match(r"^- (\w+): `([^`]*)`", line.strip())
             if m:
                 fields[m.group(1)] = m.group(2)
-    if fields.get("kernel_source_sha256") != kernel_source_digest():
+    if fields.get("mask") != mask_label:
+        return None
+    if fields.get("kernel_source_sha256") != kernel_source_digest(source):
         return None
     try:
         return int(fields["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def copy_calibration(dev):
+    """One plain 256 MiB device-to-device copy: HBM counters on it give the scale factors."""
+    import torch
+
+    a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
 
 
 def cpu_baseline(cfg, Q, K, V, words, budget_rows=None):
@@ -211,12 +226,7 @@ def main(argv=None):
             e2.record(stream)
 
     if args.copy_calibration:
-        a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-        b = torch.empty_like(a)
-        torch.cuda.synchronize()
-        b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
+        copy_calibration(dev)
 
     for _ in range(args.warmup):
         step()
@@ -295,7 +305,7 @@ def main(argv=None):
                       "attention_min": round(min(attn_ms), 4)},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": round(peak, 2),
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                     "traffic": None if args.fused else recorded_traffic(cfg.name),
+                     "traffic": None if args.fused else recorded_traffic(f"routed_attn_fwd_{cfg.name}", mask_label),
                      "kernel": (f"v_tiles_kernel + routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1, true>"
                                 if args.fused else f"routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1>"),
                      "peak_note": "precision-weighted: QK^T FP16 share at 2.5 PFLOP/s, INT8 share at "
@@ -337,6 +347,8 @@ def bench_decode(args, cfg, mask):
     stream = torch.cuda.current_stream()
     run = lambda: tm.tilemix_decode(q1, k, K8, dK, V8, dV, w, cfg.group_size, cfg.scale, O=O,
                                     workspace=ws, stream=stream, route_hint=hint)
+    if args.copy_calibration:
+        copy_calibration(dev)
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
@@ -368,7 +380,8 @@ def bench_decode(args, cfg, mask):
                    "d": cfg.d, "L_k": cfg.L, "group_size": cfg.group_size, "mask": mask.label,
                    "int8_key_share": round(float(bits.mean()), 4)},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": 8000.0, "unit": "GB/s",
-                     "frac": round(gbs / 8000.0, 4), "traffic": None,
+                     "frac": round(gbs / 8000.0, 4),
+                     "traffic": recorded_traffic(f"decode_{cfg.name}", mask.label, "decode.hip"),
                      "kernel": "decode_partial_kernel + decode_combine_kernel (event-timed step)"},
     }
     print(json.dumps(line), flush=True)
