@@ -15,3 +15,25 @@ def test_more_than_one_gpu_is_refused():
     assert out.returncode == 2
     line = json.loads(out.stdout.strip().splitlines()[-1])
     assert line["n_gpus"] == 2 and "one GPU" in line["error"]
+
+
+def test_recorded_traffic_needs_matching_mask_and_source():
+    """roofline.traffic comes from a committed counter summary only for the mask and kernel
+    source it was taken on."""
+    sys.path.insert(0, ROOT)
+    import bench
+
+    for profile, source in (("routed_attn_fwd_32k-gqa", "attn_fwd.hip"),
+                            ("decode_64k-b4-gqa", "decode.hip")):
+        path = os.path.join(ROOT, "profiles", f"{profile}_hbm_traffic.md")
+        fields = dict(line[2:].split(": ", 1) for line in open(path) if line.startswith("- "))
+        mask = fields["mask"].strip().strip("`")
+        want = int(fields["traffic_bytes_per_launch"].strip().strip("`"))
+        digest = fields["kernel_source_sha256"].strip().strip("`")
+        got = bench.recorded_traffic(profile, mask, source)
+        if digest == bench.kernel_source_digest(source):
+            assert got == want
+        else:
+            assert got is None
+        assert bench.recorded_traffic(profile, mask + "-other", source) is None
+    assert bench.recorded_traffic("no-such-profile", "bern0.5") is None
