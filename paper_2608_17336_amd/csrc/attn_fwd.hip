@@ -424,6 +424,70 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     need_fp16 = __any((~my_word & valid) != 0ull);
   }
 
+  // Tile sources (uniform bases).
+  const int kstride = a.Hk * D * 2;                              // bytes between keys (FP16)
+  const char* kbase = reinterpret_cast<const char*>(a.K) + ((size_t)k_row0 * a.Hk + hk) * D * 2;
+  const char* k8base = reinterpret_cast<const char*>(a.K8) + ((size_t)k_row0 * a.Hk + hk) * D;
+  const char* vbase = reinterpret_cast<const char*>(a.Vt) + (size_t)vt_tile0 * (size_t)(D * kBlockN * 2);
+  const DmaPlan<C::kKRow> plan_k(lane, kstride);
+  const DmaPlan<C::kK8Row> plan_k8(lane, kstride / 2);
+  const DmaPlan<C::kVRow> plan_v(lane, C::kVRow);
+  auto k_slot = [](int n) { return (n & 1) * C::kKBytes; };                   // LDS offsets
+  auto v_slot = [](int n) { return 2 * C::kKBytes + (n & 1) * C::kVBytes; };
+  const uint32_t smem_lds = lds_addr_of(smem);
+
+  // Copies are issued in tile order, K and V each on their own.  The issue state advances by
+  // additions only: the next tile, its routing group (tile = group * g + r) and its source
+  // addresses.  The route of every issued K tile is kept in a 64-bit ring (bit t mod 64),
+  // which the math reads back; at most two K tiles are ever in flight.
+  int iss_kt = 0, iss_vt = 0, iss_g = 0, iss_r = 0;
+  uint64_t route_ring = 0;
+  const char* iss_k = kbase;
+  const char* iss_k8 = k8base;
+  const char* iss_v = vbase;
+  auto issue_k_next = [&]() {
+    const bool int8 = group_route(iss_g);
+    const uint64_t bit = 1ull << (iss_kt & 63);
+    route_ring = int8 ? (route_ring | bit) : (route_ring & ~bit);
+    const uint32_t dst = smem_lds + (uint32_t)k_slot(iss_kt);
+    const int rows = min(kBlockN, Lk - iss_kt * kBlockN);
+    if (int8 && !OTF)   // OTF stages every key tile in FP16
+      dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(iss_k8, kstride / 2, rows, dst, wave, lane, plan_k8);
+    else   // 8 copies per 64-channel half of the FP16 key tile
+      dma_tile<C::kKRow, C::kKInstr, kBlockN, 8, 128>(iss_k, kstride, rows, dst, wave, lane, plan_k);
+    ++iss_kt;
+    if (++iss_r == a.g) {
+      iss_r = 0;
+      ++iss_g;
+    }
+    iss_k += (size_t)kBlockN * kstride;
+    iss_k8 += (size_t)kBlockN * (kstride / 2);
+  };
+  auto issue_v_next = [&]() {
+    dma_tile<C::kVRow, C::kVInstr, D>(iss_v, C::kVRow, D, smem_lds + (uint32_t)v_slot(iss_vt), wave,
+                                      lane, plan_v);
+    ++iss_vt;
+    iss_v += (size_t)D * kBlockN * 2;
+  };
+  // Every sync below frees exactly one K and one V slot, so at most one tile of each kind is
+  // pending at a call.
+  auto issue = [&](int k_last, int v_last) {
+    if (iss_kt <= min(k_last, n_end)) issue_k_next();
+    if (iss_vt <= min(v_last, n_end)) issue_v_next();
+  };
+  auto route_of = [&](int n) -> bool { return (route_ring >> (n & 63)) & 1ull; };   // issued K n
+  // Every copy issued so far has landed for every wave, then K through k_last and V through
+  // v_last are issued.  Each call site issues exactly the tiles whose slots the barrier freed.
+  auto sync = [&](int k_last, int v_last) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    issue(k_last, v_last);
+  };
+  // The first K and V tiles start copying now, so that their latency overlaps the query
+  // operand set-up below.
+  issue(0, 0);   // K and V of tile 0, then K of tile 1
+  issue(1, 0);
+
   // Q operands of this wave, kept in registers for the whole row.
   half8 qf[D / 16];
   i32x4 q8f[D / 32];
@@ -527,65 +591,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
       key_scale[t] = a.dK[(size_t)(kblk0 + t) * a.Hk + hk];
   }
 
-  // Tile sources (uniform bases) and per-lane LDS fragment offsets.
-  const int kstride = a.Hk * D * 2;                              // bytes between keys (FP16)
-  const char* kbase = reinterpret_cast<const char*>(a.K) + ((size_t)k_row0 * a.Hk + hk) * D * 2;
-  const char* k8base = reinterpret_cast<const char*>(a.K8) + ((size_t)k_row0 * a.Hk + hk) * D;
-  const char* vbase = reinterpret_cast<const char*>(a.Vt) + (size_t)vt_tile0 * (size_t)(D * kBlockN * 2);
-  const DmaPlan<C::kKRow> plan_k(lane, kstride);
-  const DmaPlan<C::kK8Row> plan_k8(lane, kstride / 2);
-  const DmaPlan<C::kVRow> plan_v(lane, C::kVRow);
-  auto k_slot = [](int n) { return (n & 1) * C::kKBytes; };                   // LDS offsets
-  auto v_slot = [](int n) { return 2 * C::kKBytes + (n & 1) * C::kVBytes; };
-  const uint32_t smem_lds = lds_addr_of(smem);
-
-  // Copies are issued in tile order, K and V each on their own.  The issue state advances by
-  // additions only: the next tile, its routing group (tile = group * g + r) and its source
-  // addresses.  The route of every issued K tile is kept in a 64-bit ring (bit t mod 64),
-  // which the math reads back; at most two K tiles are ever in flight.
-  int iss_kt = 0, iss_vt = 0, iss_g = 0, iss_r = 0;
-  uint64_t route_ring = 0;
-  const char* iss_k = kbase;
-  const char* iss_k8 = k8base;
-  const char* iss_v = vbase;
-  auto issue_k_next = [&]() {
-    const bool int8 = group_route(iss_g);
-    const uint64_t bit = 1ull << (iss_kt & 63);
-    route_ring = int8 ? (route_ring | bit) : (route_ring & ~bit);
-    const uint32_t dst = smem_lds + (uint32_t)k_slot(iss_kt);
-    const int rows = min(kBlockN, Lk - iss_kt * kBlockN);
-    if (int8 && !OTF)   // OTF stages every key tile in FP16
-      dma_tile<C::kK8Row, C::kK8Instr, kBlockN>(iss_k8, kstride / 2, rows, dst, wave, lane, plan_k8);
-    else   // 8 copies per 64-channel half of the FP16 key tile
-      dma_tile<C::kKRow, C::kKInstr, kBlockN, 8, 128>(iss_k, kstride, rows, dst, wave, lane, plan_k);
-    ++iss_kt;
-    if (++iss_r == a.g) {
-      iss_r = 0;
-      ++iss_g;
-    }
-    iss_k += (size_t)kBlockN * kstride;
-    iss_k8 += (size_t)kBlockN * (kstride / 2);
-  };
-  auto issue_v_next = [&]() {
-    dma_tile<C::kVRow, C::kVInstr, D>(iss_v, C::kVRow, D, smem_lds + (uint32_t)v_slot(iss_vt), wave,
-                                      lane, plan_v);
-    ++iss_vt;
-    iss_v += (size_t)D * kBlockN * 2;
-  };
-  // Every sync below frees exactly one K and one V slot, so at most one tile of each kind is
-  // pending at a call.
-  auto issue = [&](int k_last, int v_last) {
-    if (iss_kt <= min(k_last, n_end)) issue_k_next();
-    if (iss_vt <= min(v_last, n_end)) issue_v_next();
-  };
-  auto route_of = [&](int n) -> bool { return (route_ring >> (n & 63)) & 1ull; };   // issued K n
-  // Every copy issued so far has landed for every wave, then K through k_last and V through
-  // v_last are issued.  Each call site issues exactly the tiles whose slots the barrier freed.
-  auto sync = [&](int k_last, int v_last) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    issue(k_last, v_last);
-  };
+  // Per-lane LDS fragment offsets.
   const FragOffsets<128> fo_128(lane);      // K (FP16 halves), V^T, and K8 when d = 128
   const FragOffsets<C::kK8Row> fo_k8(lane);
 
@@ -817,12 +823,10 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   const int wg_first_row_last_key = min(Lk - 1, m * BM + off);
   const int n_split = max(0, min(n_end + 1, (wg_first_row_last_key + 1) / kBlockN));
 
-  issue(0, 0);   // K and V of tile 0, then K of tile 1
-  issue(1, 0);
-  wait_all_memory();
+  wait_all_memory();   // tiles 0 and 1, issued before the query set-up
   __syncthreads();
 
-  f32x16 xa0, xa1, xb0, xb1;   // the two score buffers
+  f32x16 xa0, xa1, xb0 = {}, xb1 = {};   // the two score buffers
   uint16_t ks0 = 0;
   if constexpr (OTF) {
     if (n_split > 0 && route_of(0)) ks0 = convert_k(k_slot(0));
