@@ -58,6 +58,8 @@ __device__ __forceinline__ float pair_sum(float x) {
 // base and lds_addr pass through readfirstlane (a no-op on values the compiler already holds in
 // scalar registers), so that the scalar operands stay scalar where its uniformity analysis
 // loses track of them.
+// m0 is a register the compiler reserves (it warns that the clobber names one); the code it
+// generates for these kernels never reads m0, so setting it here disturbs nothing else.
 __device__ __forceinline__ void dma_16(const void* base, uint32_t voff, uint32_t lds_addr) {
   const uint64_t b = (uint64_t)(uintptr_t)base;
   const uint64_t bs = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b >> 32)) << 32) |
