@@ -153,7 +153,7 @@ def main(argv=None):
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; the routed attention "
+        print(json.dumps({"error": "bench.py runs on exactly one GPU; the routed attention "
                                    "path shards by (batch, KV head) with no communication, "
                                    "but multi-GPU runs are not part of it", "n_gpus": args.gpus}))
         return 2

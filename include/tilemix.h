@@ -58,7 +58,7 @@ typedef enum tilemix_status {
   TILEMIX_OK = 0,
   TILEMIX_ERR_NULL = 1,         /* a required pointer is NULL */
   TILEMIX_ERR_SHAPE = 2,        /* sizes inconsistent or out of range */
-  TILEMIX_ERR_UNSUPPORTED = 3,  /* d, tile shape or flags this build does not implement */
+  TILEMIX_ERR_UNSUPPORTED = 3,  /* d, tile shape or flags the library does not implement */
   TILEMIX_ERR_ALIGN = 4,        /* a pointer is not aligned as required */
   TILEMIX_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than tilemix_workspace_size() */
   TILEMIX_ERR_HIP = 6           /* the HIP runtime rejected a launch */

@@ -9,7 +9,7 @@ Follows Section 3.2 and Appendix C ("Blockwise INT8 Quantization",
   * codes are the nearest integers to x / scale, within [-127, 127];
   * the scale is stored in the operand dtype (FP16).
 
-Readings where the paper is silent (each also listed in the design doc):
+Readings where the paper is silent:
   * nearest-integer conversion rounds half to even;
   * x / scale is an IEEE FP32 division (not a reciprocal multiply);
   * codes are clamped to [-127, 127] after rounding;

@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kPrepThreads) void quantize_blocks_kernel(
     }
   }
   amax = block_max(amax, red);
-  const float d32 = amax / 127.0f;   // IEEE FP32 division (no fast-math in this build)
+  const float d32 = amax / 127.0f;   // IEEE FP32 division (compiled without fast-math)
 
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {

@@ -1,5 +1,5 @@
 """bench.py's command-line contract that needs no GPU: more than one GPU is refused with a
-message (this build measures one GPU), before anything touches a device."""
+message (the benchmark measures one GPU), before anything touches a device."""
 
 import json
 import os
