@@ -113,8 +113,9 @@ tilemix_status tilemix_prefill(const tilemix_params* params,
  * no K8 / scale tensors and no quantization pass.  The kernel computes the scales and codes
  * on chip, only for what INT8-routed groups use: each workgroup quantizes the 128-row query
  * block of its rows once (as tilemix_prefill does too), and every INT8-routed 64-key tile (one
- * key scale block) after its FP16 copy reaches LDS.  Codes and scales equal those of tilemix_quantize, so the output
- * equals tilemix_prefill's bit for bit.  Arguments as in tilemix_prefill; the workspace
+ * key scale block) after its FP16 copy reaches LDS.  Codes and scales equal those of
+ * tilemix_quantize, so the output equals tilemix_prefill's bit for bit.  Arguments as in
+ * tilemix_prefill; the workspace
  * (tilemix_fused_workspace_size bytes) holds only V laid out per 64-key tile.  The INT8 route
  * costs more per tile here (every workgroup requantizes the key tiles it reads); the mode
  * trades that time for the K8 scratch.
@@ -175,6 +176,42 @@ tilemix_status tilemix_debug_qk_int32(const tilemix_params* params, const int8_t
                                       const int8_t* K8, const int32_t* tiles, int32_t count,
                                       int32_t* out, void* stream);
 
+/*
+ * tilemix_debug_prefill -- a test entry point: tilemix_prefill (fused = 0) or
+ * tilemix_prefill_fused (fused = 1), fixed-length (total_q < 0; the varlen arguments are then
+ * ignored) or over a variable-length batch (as tilemix_prefill_varlen[_fused]), run by a
+ * kernel instantiation that also writes out the INT8 operands it makes and multiplies
+ * (Appendix C, "Quantization Granularity" and "INT8 Score Computation"), so that they can be
+ * compared bit for bit with an independent implementation.  O is written as by the ordinary
+ * call.  A query-tile row r is b * T_m + m for a fixed-length batch and the routing row index
+ * (the rows of sequence b after those of b - 1) for a variable-length one; R is their number.
+ *   q8     device int8, the shape of Q: the INT8 codes of each query row whose tile row has an
+ *          INT8-routed group, as the kernel's prologue made them from Q (other rows untouched)
+ *   dq     device FP16 bits [R, H_q]: the query-block scale the workgroup of (r, h_q) used, for
+ *          tile rows with an INT8-routed group (others untouched)
+ *   tiles  device int32 [R, H_q, T_n, BLOCK_M, 64]: for every INT8-routed tile the kernel
+ *          visits, C = Q8 K8^T as its accumulators held it (entries past L_q or L_k
+ *          unspecified; tiles not on the INT8 route untouched)
+ *   kinds  device int32 [R, H_q, T_n, BLOCK_M / 32]: per 32-row wave of such a tile, 1 = the
+ *          pipelined products started from the 1.5 * 2^23 bias, 2 = started from 0, 3 = the
+ *          per-tile path of tiles crossing the diagonal or the sequence end (untouched for
+ *          tiles not on the INT8 route)
+ * The caller pre-fills the export buffers so that untouched entries can be recognised.
+ */
+typedef struct tilemix_debug_export {
+  int8_t* q8;
+  uint16_t* dq;
+  int32_t* tiles;
+  int32_t* kinds;
+} tilemix_debug_export;
+
+tilemix_status tilemix_debug_prefill(const tilemix_params* params, int32_t fused, int32_t total_q,
+                                     int32_t total_k, const int32_t* cu_seqlens_q,
+                                     const int32_t* cu_seqlens_k, const void* Q, const void* K,
+                                     const void* V, const uint64_t* route_bits, int32_t route_rows,
+                                     void* O, void* workspace, size_t workspace_bytes,
+                                     const tilemix_debug_export* dbg, void* stream);
+
 /* ------------------------------------------------------------ variable-length batching
  * A batch of B sequences of different lengths, packed without padding (Section 4.1: flattened
  * inputs with cu_seqlens prefix sums; Appendix C: per-sequence scale blocks).
@@ -188,10 +225,13 @@ tilemix_status tilemix_debug_qk_int32(const tilemix_params* params, const int8_t
  *                   them only on the device; out-of-range entries are clamped so that every
  *                   access stays inside the tensors, with unspecified output.
  *   Q, O            device FP16 [total_q, H_q, d];  K, V device FP16 [total_k, H_k, d]
- *   route_bits      device uint64 [sum_b ceil(L_q,b / BLOCK_M), H_k, W]: the routing rows of
- *                   sequence b follow those of sequence b - 1; W = tilemix_route_words_per_row
- *                   (params), i.e. from the maximum key length; group bits as for
- *                   tilemix_prefill against that sequence's own legal groups
+ *   route_bits      device uint64 [route_rows, H_k, W]: the routing rows of sequence b
+ *                   (ceil(L_q,b / BLOCK_M) of them) follow those of sequence b - 1;
+ *                   W = tilemix_route_words_per_row(params), i.e. from the maximum key length;
+ *                   group bits as for tilemix_prefill against that sequence's own legal groups
+ *   route_rows      rows of route_bits (>= 0).  From the first sequence whose routing rows
+ *                   would run past them on, sequences are treated as empty: their O rows are
+ *                   not written
  *   workspace       >= tilemix_varlen_workspace_size() bytes, 256-byte aligned
  * Each sequence is attended on its own: bottom-right causal alignment with its own lengths,
  * quantization blocks restart at its first row (Appendix C varlen scale layout).
@@ -202,8 +242,29 @@ tilemix_status tilemix_varlen_workspace_size(const tilemix_params* params, int32
 tilemix_status tilemix_prefill_varlen(const tilemix_params* params, int32_t total_q,
                                       int32_t total_k, const int32_t* cu_seqlens_q,
                                       const int32_t* cu_seqlens_k, const void* Q, const void* K,
-                                      const void* V, const uint64_t* route_bits, void* O,
-                                      void* workspace, size_t workspace_bytes, void* stream);
+                                      const void* V, const uint64_t* route_bits,
+                                      int32_t route_rows, void* O, void* workspace,
+                                      size_t workspace_bytes, void* stream);
+
+/*
+ * tilemix_prefill_varlen_fused -- tilemix_prefill_varlen in the fused on-the-fly operand mode
+ * (Appendix D, "Storage and Execution Layout"; Section 4.1 prefix-sum metadata): no K8 or scale
+ * tensors; each workgroup quantizes its sequence's 128-row query block (restarting at the
+ * sequence's first row) and every INT8-routed key tile on chip, with the codes and scales of
+ * the quantize-once rule, so the output equals tilemix_prefill_varlen's bit for bit.
+ * Arguments as for tilemix_prefill_varlen; the workspace (tilemix_varlen_fused_workspace_size
+ * bytes) holds the sequence table and V laid out per 64-key tile.
+ */
+tilemix_status tilemix_varlen_fused_workspace_size(const tilemix_params* params, int32_t total_q,
+                                                   int32_t total_k, size_t* bytes);
+
+tilemix_status tilemix_prefill_varlen_fused(const tilemix_params* params, int32_t total_q,
+                                            int32_t total_k, const int32_t* cu_seqlens_q,
+                                            const int32_t* cu_seqlens_k, const void* Q,
+                                            const void* K, const void* V,
+                                            const uint64_t* route_bits, int32_t route_rows,
+                                            void* O, void* workspace, size_t workspace_bytes,
+                                            void* stream);
 
 /* --------------------------------------------------------------- INT8 key/value cache decode
  * Appendix C, "Additional Execution Interfaces": an INT8 key/value cache holds K8 and V8 with

@@ -37,6 +37,9 @@ __all__ = [
     "tilemix_fit_template",
     "tilemix_varlen_workspace_size",
     "tilemix_prefill_varlen",
+    "tilemix_varlen_fused_workspace_size",
+    "tilemix_prefill_varlen_fused",
+    "tilemix_debug_prefill",
     "tilemix_quantize_kv",
     "tilemix_decode_workspace_size",
     "tilemix_decode",
@@ -60,6 +63,9 @@ EXPORTED_SYMBOLS = (
     "tilemix_fit_template",
     "tilemix_varlen_workspace_size",
     "tilemix_prefill_varlen",
+    "tilemix_varlen_fused_workspace_size",
+    "tilemix_prefill_varlen_fused",
+    "tilemix_debug_prefill",
     "tilemix_quantize_kv",
     "tilemix_decode_workspace_size",
     "tilemix_decode",
@@ -172,6 +178,11 @@ class Template:
                         t.sp_stride, t.sp_tail, t.seed)
 
 
+class _CDebugExport(ctypes.Structure):
+    _fields_ = [("q8", ctypes.c_void_p), ("dq", ctypes.c_void_p), ("tiles", ctypes.c_void_p),
+                ("kinds", ctypes.c_void_p)]
+
+
 _LIB = None
 
 
@@ -214,9 +225,19 @@ def load_library() -> ctypes.CDLL:
     lib.tilemix_varlen_workspace_size.argtypes = [P, ctypes.c_int32, ctypes.c_int32,
                                                   ctypes.POINTER(ctypes.c_size_t)]
     lib.tilemix_varlen_workspace_size.restype = ctypes.c_int
-    lib.tilemix_prefill_varlen.argtypes = [P, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp, vp, vp,
-                                           vp, vp, ctypes.c_size_t, vp]
+    varlen_args = [P, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp, vp, vp, ctypes.c_int32, vp, vp,
+                   ctypes.c_size_t, vp]
+    lib.tilemix_prefill_varlen.argtypes = varlen_args
     lib.tilemix_prefill_varlen.restype = ctypes.c_int
+    lib.tilemix_varlen_fused_workspace_size.argtypes = [P, ctypes.c_int32, ctypes.c_int32,
+                                                        ctypes.POINTER(ctypes.c_size_t)]
+    lib.tilemix_varlen_fused_workspace_size.restype = ctypes.c_int
+    lib.tilemix_prefill_varlen_fused.argtypes = varlen_args
+    lib.tilemix_prefill_varlen_fused.restype = ctypes.c_int
+    lib.tilemix_debug_prefill.argtypes = [P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp, vp,
+                                          vp, vp, vp, vp, ctypes.c_int32, vp, vp, ctypes.c_size_t,
+                                          ctypes.POINTER(_CDebugExport), vp]
+    lib.tilemix_debug_prefill.restype = ctypes.c_int
     lib.tilemix_quantize_kv.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
     lib.tilemix_quantize_kv.restype = ctypes.c_int
     lib.tilemix_decode_workspace_size.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
@@ -252,6 +273,17 @@ def _stream(stream):
     if stream is None:
         stream = torch.cuda.current_stream()
     return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _alloc(stream, *args, **kw):
+    """torch.empty for a buffer the library uses on ``stream``: allocated while that stream is
+    current, so that the caching allocator hands the block to no other stream's allocation
+    before the work enqueued on ``stream`` is done with it."""
+    import torch
+    if stream is None:
+        return torch.empty(*args, **kw)
+    with torch.cuda.stream(stream):
+        return torch.empty(*args, **kw)
 
 
 def tilemix_route_words_per_row(params: Params) -> int:
@@ -291,24 +323,26 @@ def _check_inputs(p: Params, Q, K, V=None):
         _require(V, torch.float16, (p.batch, p.len_k, p.heads_kv, p.head_dim), "V")
 
 
-def _workspace(p: Params, workspace, device, fused: bool = False):
+def _workspace(p: Params, workspace, device, fused: bool = False, stream=None, need=None):
     import torch
-    need = tilemix_fused_workspace_size(p) if fused else tilemix_workspace_size(p)
+    if need is None:
+        need = tilemix_fused_workspace_size(p) if fused else tilemix_workspace_size(p)
     if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+        workspace = _alloc(stream, need, dtype=torch.uint8, device=device)
     nbytes = workspace.numel() * workspace.element_size()
     if nbytes < need:
         raise ValueError(f"workspace too small: {need} bytes needed")
     return workspace, nbytes
 
 
-def _route_and_out(p: Params, Q, route_bits, O):
+def _route_and_out(p: Params, Q, route_bits, O, stream=None):
     import torch
     W = tilemix_route_words_per_row(p)
     _require(route_bits, torch.int64, (p.batch if p.route_per_batch else 1, p.heads_kv, p.T_m, W),
              "route_bits")
     if O is None:
-        O = torch.empty((p.batch, p.len_q, p.heads_q, p.head_dim), dtype=torch.float16, device=Q.device)
+        O = _alloc(stream, (p.batch, p.len_q, p.heads_q, p.head_dim), dtype=torch.float16,
+                   device=Q.device)
     _require(O, torch.float16, (p.batch, p.len_q, p.heads_q, p.head_dim), "O")
     return O
 
@@ -322,8 +356,8 @@ def tilemix_prefill(Q, K, V, route_bits, group_size: int, tile=(128, 64), causal
     is allocated when not given."""
     p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
     _check_inputs(p, Q, K, V)
-    O = _route_and_out(p, Q, route_bits, O)
-    workspace, nbytes = _workspace(p, workspace, Q.device)
+    O = _route_and_out(p, Q, route_bits, O, stream)
+    workspace, nbytes = _workspace(p, workspace, Q.device, stream=stream)
     cp = p.c()
     _check(load_library().tilemix_prefill(
         ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace),
@@ -345,8 +379,8 @@ def tilemix_prefill_fused(Q, K, V, route_bits, group_size: int, tile=(128, 64), 
     >= tilemix_fused_workspace_size) is allocated when not given."""
     p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
     _check_inputs(p, Q, K, V)
-    O = _route_and_out(p, Q, route_bits, O)
-    workspace, nbytes = _workspace(p, workspace, Q.device, fused=True)
+    O = _route_and_out(p, Q, route_bits, O, stream)
+    workspace, nbytes = _workspace(p, workspace, Q.device, fused=True, stream=stream)
     cp = p.c()
     _check(load_library().tilemix_prefill_fused(
         ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace),
@@ -360,7 +394,7 @@ def tilemix_prepare(Q, K, V, group_size: int, tile=(128, 64), causal: bool = Tru
     """Operand preparation (quantize-once + V tile layout) into ``workspace``; returns it."""
     p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
     _check_inputs(p, Q, K, V)
-    workspace, nbytes = _workspace(p, workspace, Q.device)
+    workspace, nbytes = _workspace(p, workspace, Q.device, stream=stream)
     cp = p.c()
     _check(load_library().tilemix_prepare(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(workspace),
                                           ctypes.c_size_t(nbytes), _stream(stream)))
@@ -373,8 +407,8 @@ def tilemix_attend(Q, K, route_bits, workspace, group_size: int, tile=(128, 64),
     """Fused routed attention on a workspace filled by tilemix_prepare; returns O."""
     p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
     _check_inputs(p, Q, K)
-    O = _route_and_out(p, Q, route_bits, O)
-    workspace, nbytes = _workspace(p, workspace, Q.device)
+    O = _route_and_out(p, Q, route_bits, O, stream)
+    workspace, nbytes = _workspace(p, workspace, Q.device, stream=stream)
     cp = p.c()
     _check(load_library().tilemix_attend(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(route_bits), _ptr(O),
                                          _ptr(workspace), ctypes.c_size_t(nbytes), _stream(stream)))
@@ -389,10 +423,10 @@ def tilemix_quantize(Q, K, *, tile=(128, 64), stream=None):
     p = Params(B, Hq, Hk, Lq, Lk, d, tile[0], tile[1])
     _require(Q, torch.float16, (B, Lq, Hq, d), "Q")
     _require(K, torch.float16, (B, Lk, Hk, d), "K")
-    Q8 = torch.empty((B, Lq, Hq, d), dtype=torch.int8, device=Q.device)
-    K8 = torch.empty((B, Lk, Hk, d), dtype=torch.int8, device=Q.device)
-    dQ = torch.empty((B, -(-Lq // 128), Hq), dtype=torch.float16, device=Q.device)
-    dK = torch.empty((B, -(-Lk // 64), Hk), dtype=torch.float16, device=Q.device)
+    Q8 = _alloc(stream, (B, Lq, Hq, d), dtype=torch.int8, device=Q.device)
+    K8 = _alloc(stream, (B, Lk, Hk, d), dtype=torch.int8, device=Q.device)
+    dQ = _alloc(stream, (B, -(-Lq // 128), Hq), dtype=torch.float16, device=Q.device)
+    dK = _alloc(stream, (B, -(-Lk // 64), Hk), dtype=torch.float16, device=Q.device)
     cp = p.c()
     _check(load_library().tilemix_quantize(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(Q8), _ptr(dQ),
                                            _ptr(K8), _ptr(dK), _stream(stream)))
@@ -411,7 +445,7 @@ def tilemix_debug_qk_int32(Q8, K8, tiles, *, heads_q: int, heads_kv: int, tile=(
     _require(K8, torch.int8, (B, Lk, heads_kv, d), "K8")
     count = tiles.shape[0]
     _require(tiles, torch.int32, (count, 4), "tiles")
-    out = torch.empty((count, tile[0], tile[1]), dtype=torch.int32, device=Q8.device)
+    out = _alloc(stream, (count, tile[0], tile[1]), dtype=torch.int32, device=Q8.device)
     cp = p.c()
     _check(load_library().tilemix_debug_qk_int32(ctypes.byref(cp), _ptr(Q8), _ptr(K8), _ptr(tiles),
                                                  ctypes.c_int32(count), _ptr(out), _stream(stream)))
@@ -485,13 +519,15 @@ def tilemix_varlen_workspace_size(params: Params, total_q: int, total_k: int) ->
     return int(n.value)
 
 
-def tilemix_prefill_varlen(Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q: int, max_len_k: int,
-                           route_bits, group_size: int, tile=(128, 64), causal: bool = True,
-                           scale: float | None = None, *, O=None, workspace=None, stream=None,
-                           route_hint: int = -1):
-    """Routed prefill attention over a packed variable-length batch.  Q [total_q, Hq, d],
-    K/V [total_k, Hk, d] fp16 CUDA tensors; cu_seqlens_q/k int32 CUDA [B + 1]; route_bits the
-    uint64 words [sum_b ceil(L_q,b / BLOCK_M), Hk, W] as an int64 CUDA tensor.  Returns O."""
+def tilemix_varlen_fused_workspace_size(params: Params, total_q: int, total_k: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().tilemix_varlen_fused_workspace_size(ctypes.byref(params.c()), total_q,
+                                                              total_k, ctypes.byref(n)))
+    return int(n.value)
+
+
+def _varlen_call(name, Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q, max_len_k, route_bits,
+                 group_size, tile, causal, scale, O, workspace, stream, route_hint, fused):
     import torch
     total_q, Hq, d = Q.shape
     total_k, Hk = K.shape[0], K.shape[1]
@@ -507,19 +543,96 @@ def tilemix_prefill_varlen(Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q: int, 
         raise ValueError("route_bits must be [rows, H_k, W]")
     _require(route_bits, torch.int64, tuple(route_bits.shape), "route_bits")
     if O is None:
-        O = torch.empty((total_q, Hq, d), dtype=torch.float16, device=Q.device)
+        O = _alloc(stream, (total_q, Hq, d), dtype=torch.float16, device=Q.device)
     _require(O, torch.float16, (total_q, Hq, d), "O")
-    need = tilemix_varlen_workspace_size(p, total_q, total_k)
-    if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=Q.device)
-    nbytes = workspace.numel() * workspace.element_size()
-    if nbytes < need:
-        raise ValueError(f"workspace too small: {need} bytes needed")
+    need = (tilemix_varlen_fused_workspace_size(p, total_q, total_k) if fused
+            else tilemix_varlen_workspace_size(p, total_q, total_k))
+    workspace, nbytes = _workspace(p, workspace, Q.device, stream=stream, need=need)
     cp = p.c()
-    _check(load_library().tilemix_prefill_varlen(
+    _check(getattr(load_library(), name)(
         ctypes.byref(cp), total_q, total_k, _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), _ptr(Q), _ptr(K),
-        _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace), ctypes.c_size_t(nbytes), _stream(stream)))
+        _ptr(V), _ptr(route_bits), ctypes.c_int32(route_bits.shape[0]), _ptr(O), _ptr(workspace),
+        ctypes.c_size_t(nbytes), _stream(stream)))
     return O
+
+
+def tilemix_prefill_varlen(Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q: int, max_len_k: int,
+                           route_bits, group_size: int, tile=(128, 64), causal: bool = True,
+                           scale: float | None = None, *, O=None, workspace=None, stream=None,
+                           route_hint: int = -1):
+    """Routed prefill attention over a packed variable-length batch.  Q [total_q, Hq, d],
+    K/V [total_k, Hk, d] fp16 CUDA tensors; cu_seqlens_q/k int32 CUDA [B + 1]; route_bits the
+    uint64 words [sum_b ceil(L_q,b / BLOCK_M), Hk, W] as an int64 CUDA tensor.  Returns O."""
+    return _varlen_call("tilemix_prefill_varlen", Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q,
+                        max_len_k, route_bits, group_size, tile, causal, scale, O, workspace, stream,
+                        route_hint, False)
+
+
+def tilemix_prefill_varlen_fused(Q, K, V, cu_seqlens_q, cu_seqlens_k, max_len_q: int,
+                                 max_len_k: int, route_bits, group_size: int, tile=(128, 64),
+                                 causal: bool = True, scale: float | None = None, *, O=None,
+                                 workspace=None, stream=None, route_hint: int = -1):
+    """tilemix_prefill_varlen in the fused on-the-fly operand mode (no K8 / scale tensors)."""
+    return _varlen_call("tilemix_prefill_varlen_fused", Q, K, V, cu_seqlens_q, cu_seqlens_k,
+                        max_len_q, max_len_k, route_bits, group_size, tile, causal, scale, O,
+                        workspace, stream, route_hint, True)
+
+
+def tilemix_debug_prefill(Q, K, V, route_bits, group_size: int, tile=(128, 64), causal: bool = True,
+                          scale: float | None = None, *, fused: bool = False, cu_seqlens_q=None,
+                          cu_seqlens_k=None, max_len_q: int = 0, max_len_k: int = 0,
+                          route_per_batch: bool = False, route_hint: int = -1, stream=None):
+    """Test entry point: one prefill call (fixed-length [B, L, H, d] inputs, or packed
+    [total, H, d] ones with ``cu_seqlens_q/k`` and the maximum lengths) whose kernel also exports
+    the INT8 operands it made and multiplied.  Returns (O, q8, dq, tiles, kinds): q8 like Q
+    (pre-filled with -128), dq int16 bits [R, Hq] (pre-filled with -1), tiles int32
+    [R, Hq, T_n, BLOCK_M, 64] and kinds int32 [R, Hq, T_n, BLOCK_M // 32] (pre-filled with 0),
+    R the query-tile rows (B * T_m, or the rows of ``route_bits`` for a packed batch)."""
+    import torch
+    varlen = cu_seqlens_q is not None
+    if varlen:
+        total_q, Hq, d = Q.shape
+        total_k, Hk = K.shape[0], K.shape[1]
+        B = cu_seqlens_q.shape[0] - 1
+        p = Params(B, Hq, Hk, max_len_q, max_len_k, d, tile[0], tile[1], group_size, causal,
+                   scale if scale else 1.0 / math.sqrt(d), False, route_hint)
+        _require(Q, torch.float16, (total_q, Hq, d), "Q")
+        _require(K, torch.float16, (total_k, Hk, d), "K")
+        _require(V, torch.float16, (total_k, Hk, d), "V")
+        _require(cu_seqlens_q, torch.int32, (B + 1,), "cu_seqlens_q")
+        _require(cu_seqlens_k, torch.int32, (B + 1,), "cu_seqlens_k")
+        if route_bits.dim() != 3 or tuple(route_bits.shape[1:]) != (Hk, tilemix_route_words_per_row(p)):
+            raise ValueError("route_bits must be [rows, H_k, W]")
+        _require(route_bits, torch.int64, tuple(route_bits.shape), "route_bits")
+        rows = route_bits.shape[0]
+        O = _alloc(stream, (total_q, Hq, d), dtype=torch.float16, device=Q.device)
+        need = (tilemix_varlen_fused_workspace_size(p, total_q, total_k) if fused
+                else tilemix_varlen_workspace_size(p, total_q, total_k))
+    else:
+        p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
+        _check_inputs(p, Q, K, V)
+        O = _route_and_out(p, Q, route_bits, None, stream)
+        total_q = total_k = -1
+        rows = p.batch * p.T_m
+        need = tilemix_fused_workspace_size(p) if fused else tilemix_workspace_size(p)
+    workspace, nbytes = _workspace(p, None, Q.device, stream=stream, need=need)
+    q8 = _alloc(stream, tuple(Q.shape), dtype=torch.int8, device=Q.device)
+    dq = _alloc(stream, (rows, p.heads_q), dtype=torch.int16, device=Q.device)
+    tiles = _alloc(stream, (rows, p.heads_q, p.T_n, p.block_m, 64), dtype=torch.int32, device=Q.device)
+    kinds = _alloc(stream, (rows, p.heads_q, p.T_n, p.block_m // 32), dtype=torch.int32,
+                   device=Q.device)
+    with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream()):
+        q8.fill_(-128)
+        dq.fill_(-1)
+        tiles.zero_()
+        kinds.zero_()
+    exp = _CDebugExport(_ptr(q8), _ptr(dq), _ptr(tiles), _ptr(kinds))
+    cp = p.c()
+    _check(load_library().tilemix_debug_prefill(
+        ctypes.byref(cp), int(bool(fused)), total_q, total_k, _ptr(cu_seqlens_q), _ptr(cu_seqlens_k),
+        _ptr(Q), _ptr(K), _ptr(V), _ptr(route_bits), ctypes.c_int32(rows if varlen else 0), _ptr(O),
+        _ptr(workspace), ctypes.c_size_t(nbytes), ctypes.byref(exp), _stream(stream)))
+    return O, q8, dq, tiles, kinds
 
 
 # ------------------------------------------------------------ INT8 key/value cache decode
@@ -532,10 +645,10 @@ def tilemix_quantize_kv(K, V, *, stream=None):
     p = Params(B, Hk, Hk, 1, Lk, d)
     _require(K, torch.float16, (B, Lk, Hk, d), "K")
     _require(V, torch.float16, (B, Lk, Hk, d), "V")
-    K8 = torch.empty((B, Lk, Hk, d), dtype=torch.int8, device=K.device)
-    V8 = torch.empty((B, Hk, -(-Lk // 64), d, 64), dtype=torch.int8, device=K.device)
-    dK = torch.empty((B, -(-Lk // 64), Hk), dtype=torch.float16, device=K.device)
-    dV = torch.empty_like(dK)
+    K8 = _alloc(stream, (B, Lk, Hk, d), dtype=torch.int8, device=K.device)
+    V8 = _alloc(stream, (B, Hk, -(-Lk // 64), d, 64), dtype=torch.int8, device=K.device)
+    dK = _alloc(stream, (B, -(-Lk // 64), Hk), dtype=torch.float16, device=K.device)
+    dV = _alloc(stream, (B, -(-Lk // 64), Hk), dtype=torch.float16, device=K.device)
     cp = p.c()
     _check(load_library().tilemix_quantize_kv(ctypes.byref(cp), _ptr(K), _ptr(V), _ptr(K8), _ptr(dK),
                                               _ptr(V8), _ptr(dV), _stream(stream)))
@@ -567,14 +680,10 @@ def tilemix_decode(Q, K, K8, dK, V8, dV, route_bits, group_size: int, scale: flo
     _require(route_bits, torch.int64, (B if route_per_batch else 1, Hk, 1, tilemix_route_words_per_row(p)),
              "route_bits")
     if O is None:
-        O = torch.empty_like(Q)
+        O = _alloc(stream, tuple(Q.shape), dtype=torch.float16, device=Q.device)
     _require(O, torch.float16, (B, 1, Hq, d), "O")
-    need = tilemix_decode_workspace_size(p)
-    if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=Q.device)
-    nbytes = workspace.numel() * workspace.element_size()
-    if nbytes < need:
-        raise ValueError(f"workspace too small: {need} bytes needed")
+    workspace, nbytes = _workspace(p, workspace, Q.device, stream=stream,
+                                   need=tilemix_decode_workspace_size(p))
     cp = p.c()
     _check(load_library().tilemix_decode(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(K8), _ptr(dK), _ptr(V8),
                                          _ptr(dV), _ptr(route_bits), _ptr(O), _ptr(workspace),

@@ -340,7 +340,12 @@ __device__ __forceinline__ void exp_pair(const f32x16& x0, const f32x16& x1, flo
 // (a 128-row Q block is one or two workgroups' rows) and every INT8-routed key tile after its
 // FP16 copy lands: the tile's absmax, scale and codes (the 64-key tile is exactly one key
 // scale block) into an INT8 slot in the K8 layout, for the same INT8 products.
-template <int D, int BM, int HEADS, bool OTF = false>
+//
+// DBG: a test-only instantiation that also writes out the INT8 operands the kernel makes and
+// multiplies: each row's query codes and its workgroup's query-block scale after the prologue,
+// and the INT32 products of every INT8-routed tile as its accumulators hold them (AttnArgs
+// dbg_*).  The arithmetic is that of the ordinary instantiation.
+template <int D, int BM, int HEADS, bool OTF = false, bool DBG = false>
 __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(AttnArgs a) {
   using C = TileCfg<D, BM, HEADS>;
   static_assert(HEADS == 1, "the query-block quantization reduces over the whole workgroup");
@@ -363,6 +368,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   const uint64_t* route_row =
       a.route + (size_t)b * a.route_batch_stride + ((size_t)hk * a.T_m + m) * a.W;
   long long vt_tile0 = ((long long)b * a.Hk + hk) * a.T_n;
+  long long dbg_row = (long long)b * a.T_m + m;   // DBG: this query-tile row's export index
   if (a.seqs) {
     const int* e = a.seqs + kSeqFields * b;
     Lq = e[kSeqQLen];
@@ -372,6 +378,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     k_row0 = e[kSeqKStart];
     kblk0 = e[kSeqKBlk];
     route_row = a.route + ((size_t)(e[kSeqQTile] + m) * a.Hk + hk) * a.W;
+    dbg_row = e[kSeqQTile] + m;
     vt_tile0 = (long long)hk * a.seqs[kSeqFields * a.B + kSeqKTile] + e[kSeqKTile];
   }
 
@@ -584,6 +591,42 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
       }
     }
   }
+  if constexpr (DBG) {   // the query operands of the INT8 route, as made above
+    if (need_int8) {
+      if (row_ok) {
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s)
+          *reinterpret_cast<i32x4*>(a.dbg_q8 + qoff + 32 * s + 16 * hi) = q8f[s];
+      }
+      if (tid == 0) a.dbg_dq[dbg_row * a.Hq + hq] = __builtin_bit_cast(uint16_t, (_Float16)dq);
+    }
+  }
+  // DBG: the INT32 products of INT8-routed key tile n from this wave's 32 raw scores per lane
+  // (element i is key 32*(i/16) + acc_row(i%16, lane)): 1.5 * 2^23 + C read as FP32 when the
+  // accumulators started at the bias, the exactly converted float(C) otherwise.
+  auto dbg_tile = [&](int n, const float (&v)[32], int kind) {
+    if constexpr (DBG) {
+      const size_t t = ((size_t)dbg_row * a.Hq + hq) * a.T_n + n;
+      if (lane == 0) a.dbg_kind[t * C::kWavesPerHead + wave_in_head] = kind;
+      int32_t* out = a.dbg_tiles + t * BM * kBlockN + (size_t)(32 * wave_in_head + lq) * kBlockN;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        const int key = 32 * (i >> 4) + acc_row(i & 15, lane);
+        out[key] = kind == kDbgFolded ? __builtin_bit_cast(int, v[i]) - kMagicBits : (int)v[i];
+      }
+    }
+  };
+  auto dbg_tile2 = [&](int n, const f32x16& y0, const f32x16& y1, int kind) {
+    if constexpr (DBG) {
+      float v[32];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        v[r] = y0[r];
+        v[16 + r] = y1[r];
+      }
+      dbg_tile(n, v, kind);
+    }
+  };
   const float c_fp16 = a.scale_log2e;
   const float c_int8_q = a.scale_log2e * dq;
   if (!OTF && need_int8) {   // key-block scales of the tiles this row visits (key block = key tile)
@@ -806,10 +849,19 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     bias_cur = fold ? kMagic : 0.0f;
     k_cur = fmaf(bias_cur, c_cur, msub);
   };
-  // Whether an INT8 tile with key scale ks takes the folded bias (same decision in every lane).
-  auto fold_ok = [&](uint16_t ks) {
-    const float c = c_int8_q * half_bits_to_float(ks);
-    return !__any(!(fmaf(kMagic, c, fabsf(msub)) < kFoldLimit));
+  // Whether an INT8 tile with score factor c may carry the folded bias against the current
+  // subtrahend (the same decision in every lane of the wave).
+  auto fold_ok_c = [&](float c) { return !__any(!(fmaf(kMagic, c, fabsf(msub)) < kFoldLimit)); };
+  auto fold_ok = [&](uint16_t ks) { return fold_ok_c(c_int8_q * half_bits_to_float(ks)); };
+  // Drop the bias from a folded tile's raw scores when the running max moved past the fold's
+  // bound: raw - 1.5 * 2^23 = C exactly (both lie in [2^23, 2^24)), so the tile continues as an
+  // exactly converted one.
+  auto unfold = [&](f32x16& y0, f32x16& y1) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      y0[r] -= kMagic;
+      y1[r] -= kMagic;
+    }
   };
 
   using True = std::integral_constant<bool, true>;
@@ -842,11 +894,16 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     if (fold) phase_a(QKInt8{}, False{}, k8_off, xb0, xb1, xa0, xa1, unused_p, unused_z);
     else if (int8) phase_a(QKInt8Exact{}, False{}, k8_off, xb0, xb1, xa0, xa1, unused_p, unused_z);
     else phase_a(QKFp16{}, False{}, k_slot(0), xb0, xb1, xa0, xa1, unused_p, unused_z);
+    if (int8) dbg_tile2(0, xa0, xa1, fold ? kDbgFolded : kDbgExact);
     set_tile(int8, fold, ks0);
     raise_max((pair_max(lane_max(xa0, xa1)) - bias_cur) * c_cur);
+    if (fold && !fold_ok(ks0)) {   // the tile's own max moved the subtrahend past the bound
+      unfold(xa0, xa1);
+      set_tile(true, false, ks0);
+    }
   }
   // Step n: scores of tile n in x, tile n + 1's go to y.
-  auto step = [&](int n, const f32x16& x0, const f32x16& x1, f32x16& y0, f32x16& y1) {
+  auto step = [&](int n, f32x16& x0, f32x16& x1, f32x16& y0, f32x16& y1) {
     sync(n + 2, n + 1);   // K of tile n + 1 and V of tile n landed; K n + 2, V n + 1 in flight
     const bool has_next = n + 1 < n_split;
     const bool int8 = has_next && route_of(n + 1);
@@ -854,7 +911,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     if constexpr (OTF) ks = int8 ? convert_k(k_slot(n + 1)) : (uint16_t)0;   // whole workgroup
     else ks = key_scale[min(n + 1, n_end)];
     if (!wave_active) return;
-    const bool fold = int8 && fold_ok(ks);
+    bool fold = int8 && fold_ok(ks);
     const int k8_off = OTF ? kK8Off : k_slot(n + 1);
     half8 pfr[4];
     float zs;
@@ -869,10 +926,21 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     } else {
       phase_a(QKFp16{}, True{}, k_slot(n + 1), x0, x1, y0, y1, pfr, zs);
     }
+    if (int8) dbg_tile2(n + 1, y0, y1, fold ? kDbgFolded : kDbgExact);
     if (__builtin_expect(__any(!(zs <= kSumLimit)), 0)) {
       // Some P of tile n left the comfortable FP16 range: refresh the running max from the
-      // tile's exact max and redo its exp.
+      // tile's exact max and redo its exp.  A folded tile n or n + 1 whose bias no longer
+      // fits the fold's bound against the new subtrahend is converted exactly first.
       raise_max((pair_max(lane_max(x0, x1)) - bias_cur) * c_cur);
+      if (bias_cur != 0.0f && !fold_ok_c(c_cur)) {
+        unfold(x0, x1);
+        bias_cur = 0.0f;
+        k_cur = msub;
+      }
+      if (fold && !fold_ok(ks)) {
+        unfold(y0, y1);
+        fold = false;
+      }
       f32x16 u0, u1;
       phase_a(QKNone{}, True{}, 0, x0, x1, u0, u1, pfr, zs);
     }
@@ -898,6 +966,7 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
     if (wave_active && n * kBlockN <= wave_last_key) {
       float svm[32], c;
       qk(n, svm, c, ks_otf);
+      if (route_of(n)) dbg_tile(n, svm, kDbgMasked);
       half8 pfr[4];
       softmax_step<D, true>(svm, c, n * kBlockN, my_last_key, lane, m_run, z_run, oacc, pfr);
       pv(n, pfr);
@@ -976,8 +1045,12 @@ hipError_t launch_attn_t(const AttnArgs& a, hipStream_t stream) {
   using C = TileCfg<D, BM, HEADS>;
   const long long grid = (long long)a.B * (a.Hq / HEADS) * a.T_m;
   if (grid <= 0 || grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS, OTF>), dim3((unsigned)grid),
-                     dim3(C::kThreads), 0, stream, a);
+  if (a.dbg_tiles)
+    hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS, OTF, true>), dim3((unsigned)grid),
+                       dim3(C::kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((routed_attn_fwd_kernel<D, BM, HEADS, OTF>), dim3((unsigned)grid),
+                       dim3(C::kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -995,7 +1068,6 @@ hipError_t launch_routed_attention(const AttnArgs& a, int d, int block_m, hipStr
   // On-the-fly operands: an all-FP16 map has nothing to quantize, and the quantize-once kernel
   // then reads neither Q8 nor K8 nor their scales.
   if (a.on_the_fly && !a.force_fp16) {
-    if (a.seqs) return hipErrorInvalidValue;
     if (d == 128 && block_m == 128) return launch_attn_t<128, 128, 1, true>(a, stream);
     if (d == 128 && block_m == 64) return launch_attn_t<128, 64, 1, true>(a, stream);
     if (d == 64 && block_m == 128) return launch_attn_t<64, 128, 1, true>(a, stream);

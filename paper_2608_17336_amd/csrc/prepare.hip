@@ -182,18 +182,24 @@ namespace {
 // host never reads them: for each sequence its rows in the packed Q and K (clamped to the
 // tensors, the maximum lengths and after the previous sequence, so that a malformed table
 // stays in bounds) and the running totals of scale blocks, query-tile rows and key tiles;
-// row B holds the totals.  One thread walks the batch.
+// row B holds the totals.  Once a sequence's query-tile rows would run past the route_rows
+// routing rows the caller passed, it and every later sequence are treated as empty (no query
+// rows).  One thread walks the batch.
 __global__ void seq_table_kernel(const int* __restrict__ cu_q, const int* __restrict__ cu_k,
                                  int batch, int total_q, int total_k, int max_q, int max_k,
-                                 int block_m, int* __restrict__ seqs) {
+                                 int block_m, int route_rows, int* __restrict__ seqs) {
   if (threadIdx.x != 0) return;
   int q_end = 0, k_end = 0, qblk = 0, kblk = 0, qtile = 0, ktile = 0;
+  bool fits = true;
   for (int b = 0; b < batch; ++b) {
     const int qs = min(max(cu_q[b], q_end), total_q);
     const int qe = min(max(cu_q[b + 1], qs), total_q);
     const int ks = min(max(cu_k[b], k_end), total_k);
     const int ke = min(max(cu_k[b + 1], ks), total_k);
-    const int ql = min(qe - qs, max_q), kl = min(ke - ks, max_k);
+    int ql = min(qe - qs, max_q);
+    const int kl = min(ke - ks, max_k);
+    fits = fits && qtile + (ql + block_m - 1) / block_m <= route_rows;
+    if (!fits) ql = 0;
     int* e = seqs + kSeqFields * b;
     e[kSeqQStart] = qs; e[kSeqQLen] = ql; e[kSeqKStart] = ks; e[kSeqKLen] = kl;
     e[kSeqQBlk] = qblk; e[kSeqKBlk] = kblk; e[kSeqQTile] = qtile; e[kSeqKTile] = ktile;
@@ -212,9 +218,10 @@ __global__ void seq_table_kernel(const int* __restrict__ cu_q, const int* __rest
 }  // namespace
 
 hipError_t launch_seq_table(const int* cu_q, const int* cu_k, int batch, int total_q, int total_k,
-                            int max_q, int max_k, int block_m, int* seqs, hipStream_t stream) {
+                            int max_q, int max_k, int block_m, int route_rows, int* seqs,
+                            hipStream_t stream) {
   hipLaunchKernelGGL(seq_table_kernel, dim3(1), dim3(64), 0, stream, cu_q, cu_k, batch, total_q,
-                     total_k, max_q, max_k, block_m, seqs);
+                     total_k, max_q, max_k, block_m, route_rows, seqs);
   return hipGetLastError();
 }
 

@@ -178,7 +178,8 @@ tilemix_status prepare_impl(const tilemix_params& p, const Plan& pl, const void*
 
 tilemix_status attend_impl(const tilemix_params& p, const Plan& pl, const void* Q, const void* K,
                            const uint64_t* route_bits, void* O, const void* workspace,
-                           hipStream_t s, const int* seqs = nullptr, bool fused = false) {
+                           hipStream_t s, const int* seqs = nullptr, bool fused = false,
+                           const tilemix_debug_export* dbg = nullptr) {
   const char* ws = static_cast<const char*>(workspace);
   tilemix::AttnArgs a{};
   a.seqs = seqs;
@@ -197,6 +198,12 @@ tilemix_status attend_impl(const tilemix_params& p, const Plan& pl, const void* 
   a.on_the_fly = fused ? 1 : 0;
   a.route_batch_stride = p.route_per_batch ? (long long)p.heads_kv * pl.T_m * pl.W : 0;
   a.scale_log2e = p.scale * 1.4426950408889634f;
+  if (dbg) {
+    a.dbg_q8 = dbg->q8;
+    a.dbg_dq = dbg->dq;
+    a.dbg_tiles = dbg->tiles;
+    a.dbg_kind = dbg->kinds;
+  }
   return hip_status(tilemix::launch_routed_attention(a, p.head_dim, p.block_m, s), "routed attention");
 }
 
@@ -216,19 +223,72 @@ tilemix_status check_out(const uint64_t* route_bits, const void* O) {
 
 }  // namespace
 
+namespace {
+
+tilemix_status check_varlen(const tilemix_params* params, int32_t total_q, int32_t total_k) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  if (total_q < 1 || total_k < 1) return fail(TILEMIX_ERR_SHAPE, "total_q and total_k must be >= 1");
+  if (params->route_per_batch != 0)
+    return fail(TILEMIX_ERR_SHAPE, "route_per_batch must be 0 for a variable-length batch");
+  if ((long long)total_q * params->heads_q * params->head_dim > (1LL << 40) ||
+      (long long)total_k * params->heads_kv * params->head_dim > (1LL << 40))
+    return fail(TILEMIX_ERR_SHAPE, "tensor too large");
+  return TILEMIX_OK;
+}
+
+// A variable-length batch (total_q >= 0) or a fixed-length one (total_q < 0).
+struct Varlen {
+  int32_t total_q = -1, total_k = -1;
+  const int32_t* cu_q = nullptr;
+  const int32_t* cu_k = nullptr;
+  int32_t route_rows = 0;
+};
+
+// Every prefill entry point: validation, the workspace plan, the sequence table of a
+// variable-length batch, the operand preparation and the attention kernel.
+tilemix_status run_prefill(const tilemix_params* params, bool fused, const Varlen& vl,
+                           const void* Q, const void* K, const void* V,
+                           const uint64_t* route_bits, void* O, void* workspace,
+                           size_t workspace_bytes, void* stream,
+                           const tilemix_debug_export* dbg = nullptr) {
+  const bool varlen = vl.total_q >= 0;
+  tilemix_status st = varlen ? check_varlen(params, vl.total_q, vl.total_k) : validate(params);
+  if (st != TILEMIX_OK) return st;
+  if (varlen) {
+    if (!vl.cu_q || !vl.cu_k) return fail(TILEMIX_ERR_NULL, "cu_seqlens must be non-NULL");
+    if (!aligned(vl.cu_q, 4) || !aligned(vl.cu_k, 4))
+      return fail(TILEMIX_ERR_ALIGN, "cu_seqlens must be 4-byte aligned");
+    if (vl.route_rows < 0) return fail(TILEMIX_ERR_SHAPE, "route_rows must be >= 0");
+  }
+  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
+  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
+  const Plan pl = varlen ? make_plan(params, vl.total_q, vl.total_k, fused)
+                         : make_plan(params, -1, -1, fused);
+  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int* seqs = nullptr;
+  if (varlen) {
+    seqs = reinterpret_cast<int*>(static_cast<char*>(workspace) + pl.seq_off);
+    st = hip_status(tilemix::launch_seq_table(vl.cu_q, vl.cu_k, params->batch, vl.total_q,
+                                              vl.total_k, params->len_q, params->len_k,
+                                              params->block_m, vl.route_rows, seqs, s),
+                    "sequence table");
+    if (st != TILEMIX_OK) return st;
+  }
+  if ((st = prepare_impl(*params, pl, Q, K, V, workspace, s, seqs, fused)) != TILEMIX_OK) return st;
+  if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, s, seqs, fused, dbg)) != TILEMIX_OK)
+    return st;
+  return ok();
+}
+
+}  // namespace
+
 tilemix_status tilemix_prefill(const tilemix_params* params, const void* Q, const void* K,
                                const void* V, const uint64_t* route_bits, void* O,
                                void* workspace, size_t workspace_bytes, void* stream) {
-  tilemix_status st = validate(params);
-  if (st != TILEMIX_OK) return st;
-  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
-  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
-  const Plan pl = make_plan(params);
-  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = prepare_impl(*params, pl, Q, K, V, workspace, s)) != TILEMIX_OK) return st;
-  if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, s)) != TILEMIX_OK) return st;
-  return ok();
+  return run_prefill(params, false, Varlen{}, Q, K, V, route_bits, O, workspace, workspace_bytes,
+                     stream);
 }
 
 tilemix_status tilemix_fused_workspace_size(const tilemix_params* params, size_t* bytes) {
@@ -242,17 +302,8 @@ tilemix_status tilemix_fused_workspace_size(const tilemix_params* params, size_t
 tilemix_status tilemix_prefill_fused(const tilemix_params* params, const void* Q, const void* K,
                                      const void* V, const uint64_t* route_bits, void* O,
                                      void* workspace, size_t workspace_bytes, void* stream) {
-  tilemix_status st = validate(params);
-  if (st != TILEMIX_OK) return st;
-  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
-  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
-  const Plan pl = make_plan(params, -1, -1, true);
-  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = prepare_impl(*params, pl, Q, K, V, workspace, s, nullptr, true)) != TILEMIX_OK) return st;
-  if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, s, nullptr, true)) != TILEMIX_OK)
-    return st;
-  return ok();
+  return run_prefill(params, true, Varlen{}, Q, K, V, route_bits, O, workspace, workspace_bytes,
+                     stream);
 }
 
 tilemix_status tilemix_prepare(const tilemix_params* params, const void* Q, const void* K,
@@ -283,22 +334,6 @@ tilemix_status tilemix_attend(const tilemix_params* params, const void* Q, const
   return ok();
 }
 
-namespace {
-
-tilemix_status check_varlen(const tilemix_params* params, int32_t total_q, int32_t total_k) {
-  tilemix_status st = validate(params);
-  if (st != TILEMIX_OK) return st;
-  if (total_q < 1 || total_k < 1) return fail(TILEMIX_ERR_SHAPE, "total_q and total_k must be >= 1");
-  if (params->route_per_batch != 0)
-    return fail(TILEMIX_ERR_SHAPE, "route_per_batch must be 0 for a variable-length batch");
-  if ((long long)total_q * params->heads_q * params->head_dim > (1LL << 40) ||
-      (long long)total_k * params->heads_kv * params->head_dim > (1LL << 40))
-    return fail(TILEMIX_ERR_SHAPE, "tensor too large");
-  return TILEMIX_OK;
-}
-
-}  // namespace
-
 tilemix_status tilemix_varlen_workspace_size(const tilemix_params* params, int32_t total_q,
                                              int32_t total_k, size_t* bytes) {
   tilemix_status st = check_varlen(params, total_q, total_k);
@@ -311,26 +346,61 @@ tilemix_status tilemix_varlen_workspace_size(const tilemix_params* params, int32
 tilemix_status tilemix_prefill_varlen(const tilemix_params* params, int32_t total_q,
                                       int32_t total_k, const int32_t* cu_seqlens_q,
                                       const int32_t* cu_seqlens_k, const void* Q, const void* K,
-                                      const void* V, const uint64_t* route_bits, void* O,
-                                      void* workspace, size_t workspace_bytes, void* stream) {
+                                      const void* V, const uint64_t* route_bits,
+                                      int32_t route_rows, void* O, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  Varlen vl;
+  vl.total_q = total_q; vl.total_k = total_k;
+  vl.cu_q = cu_seqlens_q; vl.cu_k = cu_seqlens_k;
+  vl.route_rows = route_rows;
+  if (total_q < 0) return check_varlen(params, total_q, total_k);
+  return run_prefill(params, false, vl, Q, K, V, route_bits, O, workspace, workspace_bytes, stream);
+}
+
+tilemix_status tilemix_varlen_fused_workspace_size(const tilemix_params* params, int32_t total_q,
+                                                   int32_t total_k, size_t* bytes) {
   tilemix_status st = check_varlen(params, total_q, total_k);
   if (st != TILEMIX_OK) return st;
-  if (!cu_seqlens_q || !cu_seqlens_k) return fail(TILEMIX_ERR_NULL, "cu_seqlens must be non-NULL");
-  if (!aligned(cu_seqlens_q, 4) || !aligned(cu_seqlens_k, 4))
-    return fail(TILEMIX_ERR_ALIGN, "cu_seqlens must be 4-byte aligned");
-  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
-  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
-  const Plan pl = make_plan(params, total_q, total_k);
-  if ((st = check_workspace(pl, workspace, workspace_bytes)) != TILEMIX_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  int* seqs = reinterpret_cast<int*>(static_cast<char*>(workspace) + pl.seq_off);
-  st = hip_status(tilemix::launch_seq_table(cu_seqlens_q, cu_seqlens_k, params->batch, total_q,
-                                            total_k, params->len_q, params->len_k,
-                                            params->block_m, seqs, s), "sequence table");
-  if (st != TILEMIX_OK) return st;
-  if ((st = prepare_impl(*params, pl, Q, K, V, workspace, s, seqs)) != TILEMIX_OK) return st;
-  if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, s, seqs)) != TILEMIX_OK) return st;
+  if (!bytes) return fail(TILEMIX_ERR_NULL, "bytes is NULL");
+  *bytes = make_plan(params, total_q, total_k, true).total;
   return ok();
+}
+
+tilemix_status tilemix_prefill_varlen_fused(const tilemix_params* params, int32_t total_q,
+                                            int32_t total_k, const int32_t* cu_seqlens_q,
+                                            const int32_t* cu_seqlens_k, const void* Q,
+                                            const void* K, const void* V,
+                                            const uint64_t* route_bits, int32_t route_rows,
+                                            void* O, void* workspace, size_t workspace_bytes,
+                                            void* stream) {
+  Varlen vl;
+  vl.total_q = total_q; vl.total_k = total_k;
+  vl.cu_q = cu_seqlens_q; vl.cu_k = cu_seqlens_k;
+  vl.route_rows = route_rows;
+  if (total_q < 0) return check_varlen(params, total_q, total_k);
+  return run_prefill(params, true, vl, Q, K, V, route_bits, O, workspace, workspace_bytes, stream);
+}
+
+tilemix_status tilemix_debug_prefill(const tilemix_params* params, int32_t fused, int32_t total_q,
+                                     int32_t total_k, const int32_t* cu_seqlens_q,
+                                     const int32_t* cu_seqlens_k, const void* Q, const void* K,
+                                     const void* V, const uint64_t* route_bits, int32_t route_rows,
+                                     void* O, void* workspace, size_t workspace_bytes,
+                                     const tilemix_debug_export* dbg, void* stream) {
+  if (!dbg || !dbg->q8 || !dbg->dq || !dbg->tiles || !dbg->kinds)
+    return fail(TILEMIX_ERR_NULL, "every export buffer must be non-NULL");
+  if (!aligned(dbg->q8, 16) || !aligned(dbg->dq, 2) || !aligned(dbg->tiles, 4) ||
+      !aligned(dbg->kinds, 4))
+    return fail(TILEMIX_ERR_ALIGN, "q8 must be 16-byte, dq 2-byte, tiles and kinds 4-byte aligned");
+  if (fused != 0 && fused != 1) return fail(TILEMIX_ERR_SHAPE, "fused must be 0 or 1");
+  Varlen vl;
+  if (total_q >= 0) {
+    vl.total_q = total_q; vl.total_k = total_k;
+    vl.cu_q = cu_seqlens_q; vl.cu_k = cu_seqlens_k;
+    vl.route_rows = route_rows;
+  }
+  return run_prefill(params, fused == 1, vl, Q, K, V, route_bits, O, workspace, workspace_bytes,
+                     stream, dbg);
 }
 
 namespace {

@@ -48,7 +48,20 @@ struct AttnArgs {
   int on_the_fly;         // 1: no K8/scales either; the kernel quantizes INT8 key tiles on chip
   long long route_batch_stride;  // words between the maps of consecutive sequences (0 = shared)
   float scale_log2e;      // softmax scale * log2(e)
+  // Test-only export of the INT8 operands the kernel itself makes and multiplies (all nullptr
+  // in normal calls; a separate kernel instantiation writes them).  A query-tile row index r is
+  // b * T_m + m (or, in a variable-length batch, the sequence's first routing row + m).
+  int8_t* dbg_q8;         // like Q: the query codes of every row whose tile row has an INT8 group
+  uint16_t* dbg_dq;       // FP16 bits [rows r, Hq]: the query-block scale each workgroup used
+  int32_t* dbg_tiles;     // [rows r, Hq, T_n, BM, 64]: INT32 products of the INT8-routed tiles
+  int32_t* dbg_kind;      // [rows r, Hq, T_n, BM / 32]: per wave, how the tile's products were
+                          // formed (kDbg* below); untouched for tiles not on the INT8 route
 };
+
+// dbg_kind values.
+constexpr int kDbgFolded = 1;   // pipelined, accumulator started at the 1.5 * 2^23 bias
+constexpr int kDbgExact = 2;    // pipelined, accumulator started at 0
+constexpr int kDbgMasked = 3;   // the per-tile masked path
 
 // Arguments of the INT8 key/value cache decode kernels (one query token per sequence).
 constexpr int kDecMaxGroup = 16;   // query heads per KV head
@@ -87,7 +100,8 @@ hipError_t launch_quantize(const _Float16* X, int8_t* X8, uint16_t* dX, int B, i
 hipError_t launch_v_tiles(const _Float16* V, _Float16* Vt, int B, int L, int H, int d,
                           const int* seqs, hipStream_t stream);
 hipError_t launch_seq_table(const int* cu_q, const int* cu_k, int batch, int total_q, int total_k,
-                            int max_q, int max_k, int block_m, int* seqs, hipStream_t stream);
+                            int max_q, int max_k, int block_m, int route_rows, int* seqs,
+                            hipStream_t stream);
 hipError_t launch_routed_attention(const AttnArgs& args, int d, int block_m, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& args, int d, hipStream_t stream);
 int decode_chunks(int len_k);

@@ -110,3 +110,60 @@ def test_varlen_equal_lengths_matches_fixed_bitwise():
     torch.cuda.synchronize()
     np.testing.assert_array_equal(O.cpu().numpy().reshape(O_fixed.shape).view(np.uint16),
                                   O_fixed.view(np.uint16))
+
+
+@pytest.mark.parametrize("name,lens_q,lens_k,d,bm,g", CASES, ids=[c[0] for c in CASES])
+def test_varlen_fused_equals_quantize_once_bitwise(name, lens_q, lens_k, d, bm, g):
+    """The fused on-the-fly operand mode over the same packed batch (Appendix D; Section 4.1
+    prefix sums): codes and scales made on chip equal the quantize-once ones, so the output is
+    bitwise that of tilemix_prefill_varlen (checked against the oracle above); one mask is also
+    checked against the oracle directly."""
+    import torch
+    import paper_2608_17336_amd as tm
+    lens_k = lens_k or lens_q
+    Hq, Hk = 4, 2
+    B = len(lens_q)
+    total_q, total_k = sum(lens_q), sum(lens_k)
+    Lq, Lk = max(lens_q), max(lens_k)
+    cfg = small_workload("vlf", B=1, Hq=Hq, Hk=Hk, d=d, L=max(total_q, total_k), block_m=bm,
+                         group_size=g, k_outliers=True, index=900 + len(name))
+    Q, K, V = make_qkv(cfg)
+    Q, K, V = Q[0, :total_q], K[0, :total_k], V[0, :total_k]
+    p = tm.Params(B, Hq, Hk, Lq, Lk, d, bm, 64, g, True, cfg.scale)
+    W = tm.tilemix_route_words_per_row(p)
+    rng = np.random.default_rng(len(name) + 50)
+    cu_q = torch.tensor(np.concatenate([[0], np.cumsum(lens_q)]), dtype=torch.int32, device="cuda:0")
+    cu_k = torch.tensor(np.concatenate([[0], np.cumsum(lens_k)]), dtype=torch.int32, device="cuda:0")
+    q, k, v = to_dev(Q), to_dev(K), to_dev(V)
+    for p_int8 in (0.5, 1.0, 0.0):
+        words, per_seq = _pack(lens_q, lens_k, Hk, bm, g, W, rng, p_int8)
+        w = to_dev(words)
+        hint = 0 if p_int8 == 0.0 else -1
+        log(f"varlen fused {name} p_int8={p_int8}")
+        O_once = tm.tilemix_prefill_varlen(q, k, v, cu_q, cu_k, Lq, Lk, w, g, (bm, 64), True,
+                                           cfg.scale, route_hint=hint)
+        O_fused = tm.tilemix_prefill_varlen_fused(q, k, v, cu_q, cu_k, Lq, Lk, w, g, (bm, 64), True,
+                                                  cfg.scale, route_hint=hint)
+        torch.cuda.synchronize()
+        assert torch.equal(O_once.view(torch.int16), O_fused.view(torch.int16)), (name, p_int8)
+        if p_int8 == 0.5:
+            got = O_fused.float().cpu().numpy().astype(np.float64)
+            num = den = mx = 0.0
+            q0 = k0 = 0
+            for b, (lq, lk) in enumerate(zip(lens_q, lens_k)):
+                if lq:
+                    rows = [(0, h, np.arange(lq)) for h in range(Hq)]
+                    ref = routed_attention_rows(Q[None, q0:q0 + lq], K[None, k0:k0 + lk],
+                                                V[None, k0:k0 + lk], per_seq[b], block_m=bm,
+                                                block_n=64, group_size=g, causal=True,
+                                                scale=cfg.scale, rows=rows)
+                    for (_, h, idx), r in zip(rows, ref):
+                        diff = got[q0 + idx, h, :] - r
+                        mx = max(mx, float(np.abs(diff).max()))
+                        num += float((diff ** 2).sum())
+                        den += float((r ** 2).sum())
+                q0 += lq
+                k0 += lk
+            rel = (num / den) ** 0.5
+            log(f"  max_abs={mx:.3e} rel_l2={rel:.3e}")
+            assert mx <= MAX_ABS and rel <= REL_L2, (name, mx, rel)
