@@ -187,13 +187,21 @@ _LIB = None
 
 
 def load_library() -> ctypes.CDLL:
-    """Load libtilemix.so (raises if it is missing: there is no fallback path)."""
+    """Load libtilemix.so (raises if it is missing: there is no fallback path).
+
+    torch is imported first: its wheel carries its own HIP runtime under the same soname, and
+    the library then binds to that one.  Loaded the other way round, the process would hold two
+    HIP runtimes, and the library's would not see the device that torch's owns."""
     global _LIB
     if _LIB is not None:
         return _LIB
     path = library_path()
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
+    try:
+        import torch  # noqa: F401
+    except ImportError:  # pragma: no cover - host-only use of the routing templates
+        pass
     lib = ctypes.CDLL(path)
     P = ctypes.POINTER(_CParams)
     vp = ctypes.c_void_p

@@ -134,3 +134,15 @@ def test_decode_rejects_before_launch():
     assert need >= 64 * 10 * (2 + 128) * 4
     assert call(_cp(**dp), ws=ok, ws_bytes=need - 1) == 5
     assert b"needed" in lib.tilemix_last_error()
+
+
+def test_one_hip_runtime_after_load():
+    # Loading the library before torch would map a second HIP runtime (torch's wheel carries its
+    # own under the same soname), whose device list the first one owns.
+    import sys
+    code = ("import os, sys; sys.path.insert(0, %r); import paper_2608_17336_amd as tm; "
+            "tm.load_library(); maps = open('/proc/%%d/maps' %% os.getpid()).read(); "
+            "print(len({l.split()[-1] for l in maps.splitlines() if 'libamdhip64' in l}))" % ROOT)
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip().splitlines()[-1] == "1"
