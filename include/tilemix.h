@@ -108,6 +108,26 @@ tilemix_status tilemix_prefill(const tilemix_params* params,
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * tilemix_prefill_noalloc -- tilemix_prefill for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.  It
+ * allocates nothing and takes no workspace: the workspace tilemix_prefill would need lives in
+ * a device array of TILEMIX_NOALLOC_SCRATCH_BYTES (128 MiB) that the library's code object
+ * holds on each GPU it runs on until the process ends.  Problems whose
+ * tilemix_workspace_size() exceeds that are rejected with TILEMIX_ERR_WORKSPACE before
+ * anything is enqueued (the workspace takes about 3 bytes per element of K, so problems with
+ * B * L_k * H_k * d up to about 44 million fit, e.g. L_k = 32768 with 8 KV heads of d = 128).  Every call on one GPU uses
+ * that GPU's one array: calls that overlap in time on one GPU (other streams, other host
+ * threads) race and must not be issued.  Nothing in the array needs clearing between calls.
+ * Arguments, results and errors otherwise as for tilemix_prefill; the output is the same bit
+ * for bit.
+ */
+#define TILEMIX_NOALLOC_SCRATCH_BYTES (128u << 20)
+
+tilemix_status tilemix_prefill_noalloc(const tilemix_params* params,
+                                       const void* Q, const void* K, const void* V,
+                                       const uint64_t* route_bits, void* O, void* stream);
+
+/*
  * tilemix_prefill_fused -- tilemix_prefill in the fused on-the-fly operand mode (Appendix D,
  * "Storage and Execution Layout", the fused on-the-fly mode; Appendix C quantization rules):
  * no K8 / scale tensors and no quantization pass.  The kernel computes the scales and codes

@@ -24,6 +24,7 @@ __all__ = [
     "tilemix_prefill",
     "tilemix_fused_workspace_size",
     "tilemix_prefill_fused",
+    "tilemix_prefill_noalloc",
     "tilemix_prepare",
     "tilemix_attend",
     "tilemix_quantize",
@@ -52,6 +53,7 @@ EXPORTED_SYMBOLS = (
     "tilemix_prefill",
     "tilemix_fused_workspace_size",
     "tilemix_prefill_fused",
+    "tilemix_prefill_noalloc",
     "tilemix_prepare",
     "tilemix_attend",
     "tilemix_quantize",
@@ -215,6 +217,8 @@ def load_library() -> ctypes.CDLL:
     lib.tilemix_fused_workspace_size.restype = ctypes.c_int
     lib.tilemix_prefill_fused.argtypes = [P, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.tilemix_prefill_fused.restype = ctypes.c_int
+    lib.tilemix_prefill_noalloc.argtypes = [P, vp, vp, vp, vp, vp, vp]
+    lib.tilemix_prefill_noalloc.restype = ctypes.c_int
     lib.tilemix_prepare.argtypes = [P, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.tilemix_prepare.restype = ctypes.c_int
     lib.tilemix_attend.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
@@ -393,6 +397,24 @@ def tilemix_prefill_fused(Q, K, V, route_bits, group_size: int, tile=(128, 64), 
     _check(load_library().tilemix_prefill_fused(
         ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(route_bits), _ptr(O), _ptr(workspace),
         ctypes.c_size_t(nbytes), _stream(stream)))
+    return O
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20   # TILEMIX_NOALLOC_SCRATCH_BYTES
+
+
+def tilemix_prefill_noalloc(Q, K, V, route_bits, group_size: int, tile=(128, 64),
+                            causal: bool = True, scale: float | None = None, *, O, stream=None,
+                            route_per_batch: bool = False, route_hint: int = -1):
+    """tilemix_prefill with no allocation and no workspace argument: the library serves the
+    workspace from its own per-GPU device array (at most NOALLOC_SCRATCH_BYTES).  ``O`` is
+    required; nothing is allocated here either.  Calls that overlap on one GPU race."""
+    p = _prefill_params(Q, K, group_size, tile, causal, scale, route_per_batch, route_hint)
+    _check_inputs(p, Q, K, V)
+    O = _route_and_out(p, Q, route_bits, O, stream)
+    cp = p.c()
+    _check(load_library().tilemix_prefill_noalloc(
+        ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(V), _ptr(route_bits), _ptr(O), _stream(stream)))
     return O
 
 

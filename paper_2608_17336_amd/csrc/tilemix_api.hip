@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "tilemix.h"
 #include "tilemix_device.h"
 #include "tilemix_internal.h"
@@ -332,6 +334,58 @@ tilemix_status tilemix_attend(const tilemix_params* params, const void* Q, const
   if ((st = attend_impl(*params, pl, Q, K, route_bits, O, workspace, static_cast<hipStream_t>(stream))) != TILEMIX_OK)
     return st;
   return ok();
+}
+
+namespace {
+
+// The workspace of tilemix_prefill_noalloc: one file-scope device array, which the library's
+// code object holds on every GPU it is loaded on until the process ends.  Host code never
+// passes the array's name itself to a kernel (on the host it is a stand-in, not a device
+// address): it uses the address hipGetSymbolAddress returns for the current device, looked up
+// once per device on that device's first call.
+__device__ __align__(256) unsigned char scratch[TILEMIX_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+tilemix_status scratch_of_current_device(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(TILEMIX_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(TILEMIX_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return TILEMIX_OK;
+}
+
+}  // namespace
+
+tilemix_status tilemix_prefill_noalloc(const tilemix_params* params, const void* Q, const void* K,
+                                       const void* V, const uint64_t* route_bits, void* O,
+                                       void* stream) {
+  tilemix_status st = validate(params);
+  if (st != TILEMIX_OK) return st;
+  const Plan pl = make_plan(params);
+  if (pl.total > (size_t)TILEMIX_NOALLOC_SCRATCH_BYTES)
+    return fail(TILEMIX_ERR_WORKSPACE,
+                "the problem needs %zu bytes of workspace; tilemix_prefill_noalloc serves at most "
+                "%zu (use tilemix_prefill with a caller-owned workspace)",
+                pl.total, (size_t)TILEMIX_NOALLOC_SCRATCH_BYTES);
+  if ((st = check_qkv(Q, K, V)) != TILEMIX_OK) return st;
+  if ((st = check_out(route_bits, O)) != TILEMIX_OK) return st;
+  void* ws = nullptr;
+  if ((st = scratch_of_current_device(&ws)) != TILEMIX_OK) return st;
+  return run_prefill(params, false, Varlen{}, Q, K, V, route_bits, O, ws,
+                     (size_t)TILEMIX_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 tilemix_status tilemix_varlen_workspace_size(const tilemix_params* params, int32_t total_q,

@@ -136,6 +136,24 @@ def test_decode_rejects_before_launch():
     assert b"needed" in lib.tilemix_last_error()
 
 
+def test_noalloc_rejects_before_launch():
+    # Host-side checks only: every call below returns before any device call.
+    lib = tm.load_library()
+    ok = ctypes.c_void_p(0x100000)
+    big = _cp(batch=4, heads_q=64, len_q=65536, len_k=65536, group_size=8)   # 1.6 GB workspace
+    assert tm.tilemix_workspace_size(big) > tm.NOALLOC_SCRATCH_BYTES
+    st = lib.tilemix_prefill_noalloc(ctypes.byref(big.c()), ok, ok, ok, ok, ok, None)
+    assert st == 5
+    assert b"at most 134217728" in lib.tilemix_last_error()
+    small = _cp()
+    assert tm.tilemix_workspace_size(small) <= tm.NOALLOC_SCRATCH_BYTES
+    assert lib.tilemix_prefill_noalloc(ctypes.byref(small.c()), None, ok, ok, ok, ok, None) == 1
+    assert lib.tilemix_prefill_noalloc(ctypes.byref(small.c()), ok, ok, ok, ok, None, None) == 1
+    fake = ctypes.c_void_p(0x100001)
+    assert lib.tilemix_prefill_noalloc(ctypes.byref(small.c()), fake, ok, ok, ok, ok, None) == 4
+    assert lib.tilemix_prefill_noalloc(None, ok, ok, ok, ok, ok, None) == 1
+
+
 def test_one_hip_runtime_after_load():
     # Loading the library before torch would map a second HIP runtime (torch's wheel carries its
     # own under the same soname), whose device list the first one owns.
