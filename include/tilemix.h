@@ -327,6 +327,23 @@ tilemix_status tilemix_decode(const tilemix_params* params, const void* Q, const
                               const uint16_t* dV, const uint64_t* route_bits, void* O,
                               void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * tilemix_decode_varlen -- tilemix_decode over a ragged batch: sequence b's cache holds
+ * seqlens_k[b] keys (Section 4.1, per-sequence lengths; Appendix C, "Additional Execution
+ * Interfaces").  The caches keep the layouts of tilemix_decode with params.len_k as their
+ * capacity (K, K8 [B, len_k, H_k, d], V8 [B, H_k, ceil(len_k/64), d, 64], scales
+ * [B, ceil(len_k/64), H_k]); sequence b attends to its first seqlens_k[b] cached keys and the
+ * entries past them are never used.  Routing rows as for tilemix_decode, W from len_k.
+ *   seqlens_k  device int32 [B], 4-byte aligned; values are clamped to [0, len_k] on the
+ *              device; a sequence of length 0 gets O = 0
+ * Other arguments, the workspace and errors as for tilemix_decode.
+ */
+tilemix_status tilemix_decode_varlen(const tilemix_params* params, const int32_t* seqlens_k,
+                                     const void* Q, const void* K, const int8_t* K8,
+                                     const uint16_t* dK, const int8_t* V8, const uint16_t* dV,
+                                     const uint64_t* route_bits, void* O, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------ routing templates
  * Host-side routing policies of Appendix B ("Policy Construction and Sharing", "Coverage
  * Accounting" and the layouts One, Zero, Band, Global, Row-Random, Aligned Sparse, BigBird,

@@ -30,11 +30,14 @@ def kv_cache(K: np.ndarray, V: np.ndarray):
     return k8, dk, v8, dv
 
 
-def routed_decode(Q, K, k8, dk, v8, dv, words, group_size: int, scale: float) -> np.ndarray:
+def routed_decode(Q, K, k8, dk, v8, dv, words, group_size: int, scale: float,
+                  seqlens=None) -> np.ndarray:
     """O [B, 1, H_q, d] in float64 for one decode token per sequence.
 
     Q: FP16 [B, 1, H_q, d]; K: FP16 key cache [B, L_k, H_k, d] (FP16 route);
     k8/dk, v8/dv: the INT8 cache; words: uint64 [B_r, H_k, 1, W].
+    seqlens: optional per-sequence cache lengths [B]: sequence b attends to its first
+    seqlens[b] cached keys only (clamped to [0, L_k]); a sequence with none gets O = 0.
     """
     Q = np.asarray(Q)
     B, _, Hq, d = Q.shape
@@ -54,7 +57,11 @@ def routed_decode(Q, K, k8, dk, v8, dv, words, group_size: int, scale: float) ->
             c = k8[b, :, hk, :].astype(np.int64) @ q8[b, 0, hq, :].astype(np.int64)
             s8 = scale * float(dq[b, 0, hq]) * dk[b, blk, hk].astype(np.float64) * c.astype(np.float64)
             s = np.where(bits, s8, s16)
-            p = np.exp(s - s.max())
             vdeq = dv[b, blk, hk].astype(np.float64)[:, None] * v8[b, :, hk, :].astype(np.float64)
+            n = Lk if seqlens is None else min(max(int(seqlens[b]), 0), Lk)
+            if n == 0:
+                continue
+            s, vdeq = s[:n], vdeq[:n]
+            p = np.exp(s - s.max())
             out[b, 0, hq] = (p[:, None] * vdeq).sum(axis=0) / p.sum()
     return out

@@ -44,6 +44,7 @@ __all__ = [
     "tilemix_quantize_kv",
     "tilemix_decode_workspace_size",
     "tilemix_decode",
+    "tilemix_decode_varlen",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -71,6 +72,7 @@ EXPORTED_SYMBOLS = (
     "tilemix_quantize_kv",
     "tilemix_decode_workspace_size",
     "tilemix_decode",
+    "tilemix_decode_varlen",
     "tilemix_status_string",
     "tilemix_last_error",
 )
@@ -256,6 +258,8 @@ def load_library() -> ctypes.CDLL:
     lib.tilemix_decode_workspace_size.restype = ctypes.c_int
     lib.tilemix_decode.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.tilemix_decode.restype = ctypes.c_int
+    lib.tilemix_decode_varlen.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.tilemix_decode_varlen.restype = ctypes.c_int
     lib.tilemix_route_coverage.argtypes = [P, vp, ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_double)]
     lib.tilemix_route_coverage.restype = ctypes.c_int
@@ -693,9 +697,11 @@ def tilemix_decode_workspace_size(params: Params) -> int:
 
 def tilemix_decode(Q, K, K8, dK, V8, dV, route_bits, group_size: int, scale: float | None = None,
                    *, O=None, workspace=None, stream=None, route_per_batch: bool = False,
-                   route_hint: int = -1):
+                   route_hint: int = -1, seqlens_k=None):
     """One decode step: Q [B, 1, Hq, d] against the FP16 key cache K [B, L_k, H_k, d] and the
-    INT8 caches of tilemix_quantize_kv; route_bits int64 CUDA [B_r, H_k, 1, W].  Returns O."""
+    INT8 caches of tilemix_quantize_kv; route_bits int64 CUDA [B_r, H_k, 1, W].  Returns O.
+    With ``seqlens_k`` (int32 CUDA [B]) sequence b uses its first seqlens_k[b] cached keys
+    (tilemix_decode_varlen; L_k is then the caches' capacity)."""
     import torch
     B, Lq, Hq, d = Q.shape
     Lk, Hk = K.shape[1], K.shape[2]
@@ -715,6 +721,13 @@ def tilemix_decode(Q, K, K8, dK, V8, dV, route_bits, group_size: int, scale: flo
     workspace, nbytes = _workspace(p, workspace, Q.device, stream=stream,
                                    need=tilemix_decode_workspace_size(p))
     cp = p.c()
+    if seqlens_k is not None:
+        _require(seqlens_k, torch.int32, (B,), "seqlens_k")
+        _check(load_library().tilemix_decode_varlen(
+            ctypes.byref(cp), _ptr(seqlens_k), _ptr(Q), _ptr(K), _ptr(K8), _ptr(dK), _ptr(V8),
+            _ptr(dV), _ptr(route_bits), _ptr(O), _ptr(workspace), ctypes.c_size_t(nbytes),
+            _stream(stream)))
+        return O
     _check(load_library().tilemix_decode(ctypes.byref(cp), _ptr(Q), _ptr(K), _ptr(K8), _ptr(dK), _ptr(V8),
                                          _ptr(dV), _ptr(route_bits), _ptr(O), _ptr(workspace),
                                          ctypes.c_size_t(nbytes), _stream(stream)))

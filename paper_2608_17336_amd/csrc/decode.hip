@@ -22,6 +22,8 @@
 //     normalizer, unnormalized output) per (sequence, query head, chunk).
 //   decode_combine_kernel: merges the chunks of one (sequence, query head) with the
 //     log-sum-exp rule and writes O in FP16.
+// A ragged batch (per-sequence cache lengths in a padded cache) runs the same kernels: chunks
+// past a sequence's length exit at once and are not merged; a sequence with no key gets O = 0.
 #include "tilemix_device.h"
 #include "tilemix_internal.h"
 
@@ -75,8 +77,13 @@ void decode_partial_kernel(DecodeArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, lq = lane >> 4;
+  // Keys of this sequence: all L_k cached ones, or its own length in a ragged batch.  A chunk
+  // past the end has nothing to contribute and is not merged.
+  const int Lkb = a.seqlens ? min(max(a.seqlens[b], 0), a.Lk) : a.Lk;
+  if (chunk * kDecChunk >= Lkb) return;
+  const int nKBb = (Lkb + kBlockN - 1) / kBlockN;
   const int n = chunk * kDecWaves + wave;   // key tile of the wave
-  const bool live = n < a.nKB;              // the last chunk may end before its eighth tile
+  const bool live = n < nKBb;               // the last chunk may end before its eighth tile
   __shared__ __align__(16) _Float16 q16[kDecHeads][kQ16];
   __shared__ __align__(16) int8_t q8[kDecHeads][kQ8];
   __shared__ float cq[kDecHeads];                         // scale * log2(e) * dQ per head
@@ -95,7 +102,7 @@ void decode_partial_kernel(DecodeArgs a) {
     for (int e = 0; e < D / 64; ++e)
       qx[i][e] = g < G ? a.Q[((size_t)b * a.Hq + hk * G + g) * D + lane + 64 * e] : (_Float16)0.0f;
   }
-  const int nt = min(n, a.nKB - 1);
+  const int nt = min(n, nKBb - 1);
   const int gj = nt / a.g;
   const uint64_t word = a.route[((size_t)(a.route_per_batch ? b : 0) * a.Hk + hk) * a.W + (gj >> 6)];
   const bool int8 = !a.force_fp16 && ((word >> (gj & 63)) & 1ull);
@@ -110,7 +117,7 @@ void decode_partial_kernel(DecodeArgs a) {
   const char* kp[4];
 #pragma unroll
   for (int blk = 0; blk < 4; ++blk) {
-    const int key = min(kbase + 4 * blk, a.Lk - 1);   // keys past L_k are masked below
+    const int key = min(kbase + 4 * blk, Lkb - 1);    // keys past the length are masked below
     kp[blk] = kbytes + (((size_t)b * a.Lk + key) * a.Hk + hk) * row_bytes + 16 * lq;
   }
   uint4 kr[4][kS16];
@@ -189,7 +196,7 @@ void decode_partial_kernel(DecodeArgs a) {
   for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const bool ok = live && head_ok && n * kBlockN + 16 * lq + 4 * blk + r < a.Lk;
+      const bool ok = live && head_ok && n * kBlockN + 16 * lq + 4 * blk + r < Lkb;
       sc[blk][r] = ok ? sc[blk][r] : -__builtin_huge_valf();
       m = fmaxf(m, sc[blk][r]);
     }
@@ -279,6 +286,11 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeA
   constexpr int kUnroll = 8;
   const int bh = blockIdx.x;   // b * Hq + hq
   const int tid = threadIdx.x, c4 = tid % kLanes, part = tid / kLanes;
+  int chunks = a.chunks;       // the chunks that hold keys of this sequence
+  if (a.seqlens) {
+    const int len = min(max(a.seqlens[bh / a.Hq], 0), a.Lk);
+    chunks = min(chunks, (len + kDecChunk - 1) / kDecChunk);
+  }
   __shared__ float sm[kRows], sz[kRows];
   __shared__ f32x4 so[kRows][kLanes];
   const float* pm = a.part_m + (size_t)bh * a.chunks;
@@ -287,13 +299,13 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeA
   const float ninf = -__builtin_huge_valf();
   float m = ninf, z = 0.0f;
   f32x4 o = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int i0 = part; i0 < a.chunks; i0 += kRows * kUnroll) {
+  for (int i0 = part; i0 < chunks; i0 += kRows * kUnroll) {
     float mi[kUnroll], zi[kUnroll];
     f32x4 oi[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int i = i0 + u * kRows;
-      const bool ok = i < a.chunks;
+      const bool ok = i < chunks;
       mi[u] = ok ? pm[i] : ninf;
       zi[u] = ok ? pz[i] : 0.0f;
       oi[u] = ok ? po[(size_t)i * kLanes] : f32x4{0.0f, 0.0f, 0.0f, 0.0f};

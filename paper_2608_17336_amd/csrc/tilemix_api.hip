@@ -506,10 +506,12 @@ tilemix_status tilemix_decode_workspace_size(const tilemix_params* params, size_
   return ok();
 }
 
-tilemix_status tilemix_decode(const tilemix_params* params, const void* Q, const void* K,
-                              const int8_t* K8, const uint16_t* dK, const int8_t* V8,
-                              const uint16_t* dV, const uint64_t* route_bits, void* O,
-                              void* workspace, size_t workspace_bytes, void* stream) {
+namespace {
+
+tilemix_status decode_impl(const tilemix_params* params, const int32_t* seqlens_k,
+                           const void* Q, const void* K, const int8_t* K8, const uint16_t* dK,
+                           const int8_t* V8, const uint16_t* dV, const uint64_t* route_bits,
+                           void* O, void* workspace, size_t workspace_bytes, void* stream) {
   tilemix_status st = check_decode(params);
   if (st != TILEMIX_OK) return st;
   const tilemix_params& p = *params;
@@ -537,6 +539,7 @@ tilemix_status tilemix_decode(const tilemix_params* params, const void* Q, const
   a.route_per_batch = p.route_per_batch;
   a.force_fp16 = p.route_hint == 0 ? 1 : 0;
   a.scale_log2e = p.scale * 1.4426950408889634f;
+  a.seqlens = seqlens_k;
   const size_t rows = (size_t)p.batch * p.heads_q * a.chunks;
   char* ws = static_cast<char*>(workspace);
   a.part_m = reinterpret_cast<float*>(ws);
@@ -545,6 +548,27 @@ tilemix_status tilemix_decode(const tilemix_params* params, const void* Q, const
   st = hip_status(tilemix::launch_decode(a, p.head_dim, static_cast<hipStream_t>(stream)), "decode");
   if (st != TILEMIX_OK) return st;
   return ok();
+}
+
+}  // namespace
+
+tilemix_status tilemix_decode(const tilemix_params* params, const void* Q, const void* K,
+                              const int8_t* K8, const uint16_t* dK, const int8_t* V8,
+                              const uint16_t* dV, const uint64_t* route_bits, void* O,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_impl(params, nullptr, Q, K, K8, dK, V8, dV, route_bits, O, workspace,
+                     workspace_bytes, stream);
+}
+
+tilemix_status tilemix_decode_varlen(const tilemix_params* params, const int32_t* seqlens_k,
+                                     const void* Q, const void* K, const int8_t* K8,
+                                     const uint16_t* dK, const int8_t* V8, const uint16_t* dV,
+                                     const uint64_t* route_bits, void* O, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  if (!seqlens_k) return fail(TILEMIX_ERR_NULL, "seqlens_k is NULL");
+  if (!aligned(seqlens_k, 4)) return fail(TILEMIX_ERR_ALIGN, "seqlens_k must be 4-byte aligned");
+  return decode_impl(params, seqlens_k, Q, K, K8, dK, V8, dV, route_bits, O, workspace,
+                     workspace_bytes, stream);
 }
 
 tilemix_status tilemix_quantize(const tilemix_params* params, const void* Q, const void* K,

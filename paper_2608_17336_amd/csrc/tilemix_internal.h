@@ -77,6 +77,9 @@ struct DecodeArgs {
   float* part_m;           // [B, Hq, chunks]: chunk max (log2 units)
   float* part_z;           // [B, Hq, chunks]: chunk normalizer
   float* part_o;           // [B, Hq, chunks, d]: chunk output, unnormalized
+  // Per-sequence cache lengths [B] (device), or nullptr when every sequence holds Lk keys.
+  // Sequence b uses its first min(max(seqlens[b], 0), Lk) cached keys; Lk is the capacity.
+  const int* seqlens;
   int B, Hq, Hk, Lk, W, g, nKB, chunks;
   int route_per_batch, force_fp16;
   float scale_log2e;

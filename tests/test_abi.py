@@ -164,3 +164,14 @@ def test_one_hip_runtime_after_load():
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
     assert out.returncode == 0, out.stderr
     assert out.stdout.strip().splitlines()[-1] == "1"
+
+
+def test_decode_varlen_rejects_before_launch():
+    lib = tm.load_library()
+    ok = ctypes.c_void_p(0x100000)
+    cp = _cp(len_q=1, len_k=5000, heads_q=64, heads_kv=8, group_size=8).c()
+    args = [ok] * 8 + [ok, 1 << 40, None]
+    assert lib.tilemix_decode_varlen(ctypes.byref(cp), None, *args) == 1
+    assert lib.tilemix_decode_varlen(ctypes.byref(cp), ctypes.c_void_p(0x100002), *args) == 4
+    bad = _cp(len_q=2, len_k=5000, heads_q=64, heads_kv=8).c()
+    assert lib.tilemix_decode_varlen(ctypes.byref(bad), ok, *args) == 3

@@ -134,3 +134,42 @@ def test_decode_longest_cache_full_group():
     torch.cuda.synchronize()
     got = O.float().cpu().numpy().astype(np.float64)
     _check(got, routed_decode(Q1, K, *ck, words, g, cfg.scale), "L_k=262144")
+
+
+RAGGED = [
+    # B, Hq, Hk, d, capacity, g, lengths
+    (4, 8, 2, 128, 700, 2, [700, 1, 0, 333]),
+    (3, 16, 1, 128, 5000, 4, [4999, 512, 513]),
+    (2, 4, 4, 64, 300, 1, [64, 299]),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hk,d,cap,g,lens", RAGGED, ids=[str(c[-1]) for c in RAGGED])
+def test_decode_ragged_lengths(B, Hq, Hk, d, cap, g, lens):
+    """tilemix_decode_varlen: each sequence attends to the first L_b keys of a padded cache
+    (the entries past L_b hold unrelated keys and values and must not count)."""
+    import torch
+    import paper_2608_17336_amd as tm
+    cfg = small_workload("decrag", B=B, Hq=Hq, Hk=Hk, d=d, L=cap, group_size=g, k_outliers=True,
+                         index=940 + cap)
+    Q, K, V = make_qkv(cfg)
+    Q1 = np.ascontiguousarray(Q[:, -1:])
+    k, v = to_dev(K), to_dev(V)
+    K8, dK, V8, dV = tm.tilemix_quantize_kv(k, v)
+    ck = kv_cache(K, V)
+    T_mask = -(-(-(-cap // 64)) // g)
+    rng = np.random.default_rng(cap)
+    sl = torch.tensor(lens, dtype=torch.int32, device="cuda:0")
+    for p in (0.5, 0.0, 1.0):
+        words = pack_route_bits((rng.random((Hk, 1, T_mask)) < p).astype(np.uint8))
+        log(f"ragged decode lens={lens} d={d} g={g} p={p}")
+        O = tm.tilemix_decode(to_dev(Q1), k, K8, dK, V8, dV, to_dev(words), g, cfg.scale,
+                              seqlens_k=sl, route_hint=0 if p == 0.0 else -1)
+        torch.cuda.synchronize()
+        got = O.float().cpu().numpy().astype(np.float64)
+        ref = routed_decode(Q1, K, *ck, words, g, cfg.scale, seqlens=lens)
+        for b, n in enumerate(lens):
+            if n == 0:
+                assert np.all(got[b] == 0.0), b
+        nz = [b for b, n in enumerate(lens) if n > 0]
+        _check(got[nz], ref[nz], f"lens={lens} p={p}")

@@ -50,3 +50,32 @@ def test_value_quantization_error_bound():
     for (_, h, _), r in zip(rows, ref):
         err = np.abs(got[0, 0, h] - r[0]).max()
         assert 0 < err <= bound * (1 + 1e-6)
+
+
+def test_per_sequence_lengths():
+    # Sequence b attends to its first L_b cached keys.  With the cache entries past L_b set to
+    # zero, the cache's blocks that hold keys below L_b have the codes and scales of each
+    # sequence's own shorter cache, so the result must equal decoding each slice on its own;
+    # all-full lengths equal the plain call, and a length of 0 gives zeros.
+    cfg = small_workload("decvl", B=4, Hq=4, Hk=2, d=64, L=300, group_size=2, k_outliers=True,
+                         index=902)
+    Q, K, V = make_qkv(cfg)
+    Q1 = Q[:, -1:]
+    lens = [300, 1, 0, 130]
+    for b, n in enumerate(lens):
+        K[b, n:] = 0.0
+        V[b, n:] = 0.0
+    rng = np.random.default_rng(9)
+    T_mask = -(-(-(-300 // 64)) // 2)
+    words = _words(2, T_mask, rng, 0.5)
+    cache = kv_cache(K, V)
+    got = routed_decode(Q1, K, *cache, words, 2, cfg.scale, seqlens=lens)
+    for b, n in enumerate(lens):
+        if n == 0:
+            assert np.all(got[b] == 0.0)
+            continue
+        Kb, Vb = K[b:b + 1, :n], V[b:b + 1, :n]
+        ref = routed_decode(Q1[b:b + 1], Kb, *kv_cache(Kb, Vb), words, 2, cfg.scale)
+        np.testing.assert_allclose(got[b], ref[0], rtol=0, atol=1e-12)
+    full = routed_decode(Q1, K, *cache, words, 2, cfg.scale, seqlens=[300] * 4)
+    np.testing.assert_array_equal(full, routed_decode(Q1, K, *cache, words, 2, cfg.scale))
