@@ -495,14 +495,21 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   issue(0, 0);   // K and V of tile 0, then K of tile 1
   issue(1, 0);
 
-  // Q operands of this wave, kept in registers for the whole row.
+  // Q operands of this wave, kept in registers for the whole row.  The lane's 64 FP16 query
+  // values in the FP16 operand layout (lane l: row l % 32, channels 16 s + 8 (l / 32) + 0..7)
+  // are loaded once; with 128-row tiles they also give the query block's scale and codes.
   half8 qf[D / 16];
   i32x4 q8f[D / 32];
   const bool row_ok = my_q < Lq;
   const size_t qoff = ((size_t)(q_row0 + (row_ok ? my_q : 0)) * a.Hq + hq) * D;
+  constexpr bool kQBlockInRegs = BM == kQuantBlockQ;   // the workgroup's rows are one Q block
+  half8 qv[D / 16];
 #pragma unroll
   for (int s = 0; s < D / 16; ++s)
-    qf[s] = (need_fp16 && row_ok) ? as_half8(ld_global_16(a.Q + qoff + 16 * s + 8 * hi)) : half8{};
+    qv[s] = ((need_fp16 || (kQBlockInRegs && need_int8)) && row_ok)
+                ? as_half8(ld_global_16(a.Q + qoff + 16 * s + 8 * hi)) : half8{};
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) qf[s] = need_fp16 ? qv[s] : half8{};
 #pragma unroll
   for (int s = 0; s < D / 32; ++s)
     q8f[s] = i32x4{};
@@ -568,24 +575,49 @@ __global__ __launch_bounds__(HEADS * 2 * BM, 2) void routed_attn_fwd_kernel(Attn
   // quantize-once rule, and no Q8 tensor passes through HBM.
   {
     if (need_int8) {   // the same for every wave of the workgroup
-      // Q block of this row: rows qb0 .. qb0 + 127 of the sequence (those that exist).
-      const int qb0 = (m * BM / kQuantBlockQ) * kQuantBlockQ;
-      const int qrows = min(kQuantBlockQ, Lq - qb0);
       uint32_t mb = 0u;
-      for (int c = tid; c < kQuantBlockQ * (D / 8); c += C::kThreads) {
-        const int r = c / (D / 8), ch = 8 * (c % (D / 8));
-        if (r < qrows)
-          mb = absmax_bits(ld_global_16(a.Q + ((size_t)(q_row0 + qb0 + r) * a.Hq + hq) * D + ch), mb);
+      if constexpr (kQBlockInRegs) {   // the block's absmax from the values in registers
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) mb = absmax_bits(__builtin_bit_cast(uint4, qv[s]), mb);
+      } else {   // the block spans two workgroups: read it (rows qb0 .. qb0 + 127 that exist)
+        const int qb0 = (m * BM / kQuantBlockQ) * kQuantBlockQ;
+        const int qrows = min(kQuantBlockQ, Lq - qb0);
+        for (int c = tid; c < kQuantBlockQ * (D / 8); c += C::kThreads) {
+          const int r = c / (D / 8), ch = 8 * (c % (D / 8));
+          if (r < qrows)
+            mb = absmax_bits(ld_global_16(a.Q + ((size_t)(q_row0 + qb0 + r) * a.Hq + hq) * D + ch), mb);
+        }
       }
       const float amax = wg_max(bits_max_float(mb));
       const float d32 = amax / 127.0f;   // IEEE FP32 division
       const float rcp = amax > 0.0f ? 1.0f / d32 : 0.0f;
       dq = amax > 0.0f ? (float)(_Float16)d32 : 0.0f;
-      if (row_ok) {   // a zero block has rcp = 0: codes 0
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s) {
-          const uint4 c = codes16(ld_global_16(a.Q + qoff + 32 * s + 16 * hi),
-                                  ld_global_16(a.Q + qoff + 32 * s + 16 * hi + 8), d32, rcp);
+      for (int s = 0; s < D / 32; ++s) {   // codes of channels 32 s + 16 hi + 0..15
+        uint4 g0, g1;
+        if constexpr (kQBlockInRegs) {
+          // FP16 fragment 2 s + hi of this lane holds 8 of them; its partner lane (l ^ 32)
+          // holds the other 8 in its own fragment 2 s + hi, and sends it in exchange for ours.
+          const uint4 f0 = __builtin_bit_cast(uint4, qv[2 * s]);
+          const uint4 f1 = __builtin_bit_cast(uint4, qv[2 * s + 1]);
+          const uint4 mine = hi ? f1 : f0;
+          const uint4 send = hi ? f0 : f1;
+          uint32_t o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t v = e == 0 ? send.x : e == 1 ? send.y : e == 2 ? send.z : send.w;
+            const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+            o[e] = hi ? (uint32_t)r[0] : (uint32_t)r[1];   // the partner lane's value
+          }
+          const uint4 other = make_uint4(o[0], o[1], o[2], o[3]);
+          g0 = hi ? other : mine;
+          g1 = hi ? mine : other;
+        } else {
+          g0 = row_ok ? ld_global_16(a.Q + qoff + 32 * s + 16 * hi) : uint4{};
+          g1 = row_ok ? ld_global_16(a.Q + qoff + 32 * s + 16 * hi + 8) : uint4{};
+        }
+        if (row_ok) {   // a zero block has rcp = 0: codes 0
+          const uint4 c = codes16(g0, g1, d32, rcp);
           q8f[s] = i32x4{(int)c.x, (int)c.y, (int)c.z, (int)c.w};
         }
       }
