@@ -9,32 +9,37 @@
 // by HBM bandwidth; a split-K layout spreads each (sequence, KV head) stream over many
 // workgroups.
 //
-//   decode_partial_kernel<D>: workgroup (chunk of 512 keys, KV head, sequence), one 64-key
-//     tile per wave, the G <= 16 query heads of the GQA group on the columns of 16x16
-//     matrix-core tiles (padding columns carry no weight).  The tile's key rows and value
-//     rows are loaded once into registers; the group's query rows are quantized on chip (the
-//     lone decode row is a whole 128-row quantization block).  The wave scores its tile on the
-//     tile's routed path (v_mfma_i32_16x16x64_i8 on K8 rows, v_mfma_f32_16x16x32_f16 on FP16
-//     key rows); one max and one sum reduction give the chunk's max and normalizer per head;
-//     P * dV stays in registers as the FP16 operand of O^T += V^T (P dV)^T on
-//     v_mfma_f32_16x16x32_f16, V^T read from the transposed value-cache tile and widened to
-//     FP16 exactly.  The waves' partial outputs are added through LDS.  Writes (max,
-//     normalizer, unnormalized output) per (sequence, query head, chunk).
+//   decode_partial_kernel<D>: workgroup (chunk of keys, KV head, sequence), 8 waves.  The grid
+//     is sized for one 8-wave workgroup per CU (256 on an MI355X): each wave streams
+//     tiles_per_wave 64-key tiles (tile t of the chunk goes to wave t % 8, so the eight waves
+//     read neighbouring tiles at a time) and keeps its own online-softmax state (max,
+//     normalizer, output) in registers across them; the group's query heads (G <= 16) sit on
+//     the columns of 16x16 matrix-core tiles (padding columns carry no weight).  Per tile the
+//     wave issues the key rows on the routed path and the value rows together, scores the tile
+//     (v_mfma_i32_16x16x64_i8 on K8 rows, v_mfma_f32_16x16x32_f16 on FP16 key rows), and adds
+//     V^T (P dV)^T on v_mfma_f32_16x16x32_f16 with P in registers.  The group's query rows are
+//     quantized on chip once per workgroup (the lone decode row is a whole 128-row
+//     quantization block).  At the end the eight waves' states are merged through LDS with the
+//     log-sum-exp rule; the workgroup writes (max, normalizer, unnormalized output) per
+//     (sequence, query head, chunk).
 //   decode_combine_kernel: merges the chunks of one (sequence, query head) with the
 //     log-sum-exp rule and writes O in FP16.
-// A ragged batch (per-sequence cache lengths in a padded cache) runs the same kernels: chunks
-// past a sequence's length exit at once and are not merged; a sequence with no key gets O = 0.
+// A ragged batch (per-sequence cache lengths in a padded cache) runs the same kernels: tiles
+// and chunks past a sequence's length are skipped and not merged; a sequence with no key gets
+// O = 0.
 #include "tilemix_device.h"
 #include "tilemix_internal.h"
+
+#include <algorithm>
 
 namespace tilemix {
 
 namespace {
 
-constexpr int kDecWaves = 8;                        // one 64-key tile per wave
+constexpr int kDecWaves = 8;                        // waves per workgroup
 constexpr int kDecThreads = kDecWaves * kWave;      // 512
-constexpr int kDecChunk = kDecWaves * kBlockN;      // 512 keys per workgroup
 constexpr int kDecHeads = 16;                       // query heads per KV head on the MFMA columns
+constexpr int kDecSlots = 256;                      // workgroups resident at once: one per CU
 constexpr int kCombineThreads = 256;
 
 // Eight int8 codes (one per byte of v) widened to FP16, exactly: with the sign bit flipped a
@@ -56,7 +61,7 @@ __device__ __forceinline__ half8 i8x8_to_half8(uint32_t w0, uint32_t w1) {
   return out;
 }
 
-// Workgroup = (chunk of 512 keys, KV head, sequence); wave w owns key tile 8 * chunk + w.
+// Workgroup = (chunk of 8 * tiles_per_wave key tiles, KV head, sequence).
 //
 // Scores are computed transposed, S^T = K Q^T, with keys on the 16 rows and the group's query
 // heads on the 16 columns of each tile product.  Score block blk (= 2 * st + h) of a tile puts
@@ -65,8 +70,10 @@ __device__ __forceinline__ half8 i8x8_to_half8(uint32_t w0, uint32_t w1) {
 // that the B operand of P.V step st needs in lane (head, lq), slot e.  P therefore never
 // leaves the registers, and the V^T operand of step st is bytes [16 * lq + 8 * st, + 8) of a
 // channel row of the transposed value tile: one 16-byte load per lane covers both steps.
+// Registers (about 180 per lane: key rows, value rows, output, scores) allow two waves per
+// SIMD, so one 8-wave workgroup fills a CU.
 template <int D>
-__global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(4)))
+__global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void decode_partial_kernel(DecodeArgs a) {
   constexpr int kCB = D / 16;      // 16-channel blocks of the output
   constexpr int kS16 = D / 32;     // FP16 score products per 16-key block
@@ -80,20 +87,18 @@ void decode_partial_kernel(DecodeArgs a) {
   // Keys of this sequence: all L_k cached ones, or its own length in a ragged batch.  A chunk
   // past the end has nothing to contribute and is not merged.
   const int Lkb = a.seqlens ? min(max(a.seqlens[b], 0), a.Lk) : a.Lk;
-  if (chunk * kDecChunk >= Lkb) return;
+  const int tpw = a.tiles_per_wave;
+  const int tile0 = chunk * kDecWaves * tpw;   // first key tile of the chunk
+  if (tile0 * kBlockN >= Lkb) return;
   const int nKBb = (Lkb + kBlockN - 1) / kBlockN;
-  const int n = chunk * kDecWaves + wave;   // key tile of the wave
-  const bool live = n < nKBb;               // the last chunk may end before its eighth tile
   __shared__ __align__(16) _Float16 q16[kDecHeads][kQ16];
   __shared__ __align__(16) int8_t q8[kDecHeads][kQ8];
   __shared__ float cq[kDecHeads];                         // scale * log2(e) * dQ per head
   __shared__ float red_m[kDecWaves][kDecHeads], red_z[kDecWaves][kDecHeads];
   __shared__ __align__(16) float osum[kDecWaves][kDecHeads][kOS];
 
-  // 1. The group's query rows (loaded first: the quantization below waits only for them), the
-  //    routing bit and block scales of the tile (Sections 4.2, 4.3), then the key rows of its
-  //    four score blocks on the routed path.  A wave past the last tile reads the last tile
-  //    and masks all of its scores.
+  // 1. The group's query rows and this (sequence, KV head)'s routing row (Section 4.2): lane w
+  //    holds word w, so a tile's bit is a lane read plus a shift.
   _Float16 qx[kDecHeads / kDecWaves][D / 64];
 #pragma unroll
   for (int i = 0; i < kDecHeads / kDecWaves; ++i) {
@@ -102,35 +107,14 @@ void decode_partial_kernel(DecodeArgs a) {
     for (int e = 0; e < D / 64; ++e)
       qx[i][e] = g < G ? a.Q[((size_t)b * a.Hq + hk * G + g) * D + lane + 64 * e] : (_Float16)0.0f;
   }
-  const int nt = min(n, nKBb - 1);
-  const int gj = nt / a.g;
-  const uint64_t word = a.route[((size_t)(a.route_per_batch ? b : 0) * a.Hk + hk) * a.W + (gj >> 6)];
-  const bool int8 = !a.force_fp16 && ((word >> (gj & 63)) & 1ull);
-  const size_t si = ((size_t)b * a.nKB + nt) * a.Hk + hk;
-  const uint16_t dk_bits = a.dK[si], dv_bits = a.dV[si];
-  // K8 and FP16 key rows differ only in their row length (D or 2 D bytes): lane lq reads bytes
-  // 16 * lq + 64 * s of the row for product s of a 16-key block, on either path; the FP16
-  // rows need kS16 products, the K8 rows the first kS8 of them.
-  const char* kbytes = int8 ? reinterpret_cast<const char*>(a.K8) : reinterpret_cast<const char*>(a.K);
-  const size_t row_bytes = int8 ? D : 2 * D;
-  const int kbase = nt * kBlockN + 16 * (l16 >> 2) + (l16 & 3);
-  const char* kp[4];
-#pragma unroll
-  for (int blk = 0; blk < 4; ++blk) {
-    const int key = min(kbase + 4 * blk, Lkb - 1);    // keys past the length are masked below
-    kp[blk] = kbytes + (((size_t)b * a.Lk + key) * a.Hk + hk) * row_bytes + 16 * lq;
-  }
-  uint4 kr[4][kS16];
-#pragma unroll
-  for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-    for (int s = 0; s < kS8; ++s) kr[blk][s] = ld_global_16(kp[blk] + 64 * s);
-  if (!int8) {
-#pragma unroll
-    for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-      for (int s = kS8; s < kS16; ++s) kr[blk][s] = ld_global_16(kp[blk] + 64 * s);
-  }
+  const uint64_t my_word =
+      (!a.force_fp16 && lane < a.W) ? a.route[((size_t)(a.route_per_batch ? b : 0) * a.Hk + hk) * a.W + lane] : 0ull;
+  const uint32_t word_lo = (uint32_t)my_word, word_hi = (uint32_t)(my_word >> 32);
+  auto route_of = [&](int n) -> bool {
+    const int gj = n / a.g, w = gj >> 6, bit = gj & 63;
+    const uint32_t h = bit < 32 ? __builtin_amdgcn_readlane(word_lo, w) : __builtin_amdgcn_readlane(word_hi, w);
+    return (h >> (bit & 31)) & 1u;
+  };
 
   // 2. FP16 copy, INT8 codes and FP16-stored scale of the query rows (Appendix C
   //    quantization; the lone decode row forms its own 128-row block).  Rows past G are 0.
@@ -157,105 +141,131 @@ void decode_partial_kernel(DecodeArgs a) {
   }
   __syncthreads();
 
-  // 3. Scores (log2 units) of the wave's 64 keys for the 16 head columns:
-  //    v_mfma_i32_16x16x64_i8 on K8 rows or v_mfma_f32_16x16x32_f16 on FP16 key rows.
-  float sc[4][4];
-  {
-    if (int8) {
-      i32x4 qb[kS8];
-#pragma unroll
-      for (int s = 0; s < kS8; ++s) qb[s] = *reinterpret_cast<const i32x4*>(&q8[l16][64 * s + 16 * lq]);
-      const float f = cq[l16] * half_bits_to_float(dk_bits);
-#pragma unroll
-      for (int blk = 0; blk < 4; ++blk) {
-        i32x4 acc = {0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < kS8; ++s)
-          acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(as_i32x4(kr[blk][s]), qb[s], acc, 0, 0, 0);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sc[blk][r] = (float)acc[r] * f;
-      }
-    } else {
-      half8 qb[kS16];
-#pragma unroll
-      for (int s = 0; s < kS16; ++s) qb[s] = *reinterpret_cast<const half8*>(&q16[l16][32 * s + 8 * lq]);
-#pragma unroll
-      for (int blk = 0; blk < 4; ++blk) {
-        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int s = 0; s < kS16; ++s)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(kr[blk][s]), qb[s], acc, 0, 0, 0);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sc[blk][r] = acc[r] * a.scale_log2e;
-      }
-    }
-  }
+  // 3. The wave's tiles tile0 + wave, tile0 + wave + 8, ...: per tile, key rows (routed path)
+  //    and value rows are issued together; scores in log2 units; the running max, normalizer
+  //    and output of the wave are rescaled when the max grows (Section 3.1); P = 2^(s - m)
+  //    with the V block scale folded in is the FP16 B operand of the P.V products.
   const bool head_ok = l16 < G;   // columns past G are padding
-  float m = -__builtin_huge_valf();
-#pragma unroll
-  for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const bool ok = live && head_ok && n * kBlockN + 16 * lq + 4 * blk + r < Lkb;
-      sc[blk][r] = ok ? sc[blk][r] : -__builtin_huge_valf();
-      m = fmaxf(m, sc[blk][r]);
-    }
-  m = fmaxf(m, __shfl_xor(m, 16, kWave));
-  m = fmaxf(m, __shfl_xor(m, 32, kWave));
-  if (lq == 0) red_m[wave][l16] = m;
-
-  // 4. The transposed V8 tile rows of the wave's P.V products, in flight across the barrier.
-  uint4 vr[kCB];
-  {
-    const int8_t* vt = a.V8 + ((((size_t)b * a.Hk + hk) * a.nKB + nt) * D + l16) * kBlockN + 16 * lq;
-#pragma unroll
-    for (int cb = 0; cb < kCB; ++cb) vr[cb] = ld_global_16(vt + cb * 16 * kBlockN);
-  }
-  __syncthreads();
-
-  // 5. Chunk max per head; P = 2^(s - m) with the V block scale folded in (FP16 B operand);
-  //    the chunk normalizer sums P before the fold.
-  float mc = red_m[0][l16];
-#pragma unroll
-  for (int w = 1; w < kDecWaves; ++w) mc = fmaxf(mc, red_m[w][l16]);
-  const float dv = half_bits_to_float(dv_bits);
-  half8 pb[2];
-  float z = 0.0f;
-#pragma unroll
-  for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float p = sc[blk][r] == -__builtin_huge_valf() ? 0.0f : __builtin_amdgcn_exp2f(sc[blk][r] - mc);
-      z += p;
-      pb[blk >> 1][4 * (blk & 1) + r] = (_Float16)(p * dv);
-    }
-  z += __shfl_xor(z, 16, kWave);
-  z += __shfl_xor(z, 32, kWave);
-  if (lq == 0) red_z[wave][l16] = z;
-
-  // 6. O^T[channel][head] += V^T[channel][key] (P dV)^T[key][head] on
-  //    v_mfma_f32_16x16x32_f16, V^T widened to FP16 exactly.  Lane (head, lq) ends with
-  //    channels 16 * cb + 4 * lq + r of its head.
+  const float ninf = -__builtin_huge_valf();
+  float m_w = ninf, z_w = 0.0f;   // z_w: this lane's share of the normalizer
   f32x4 acc[kCB];
 #pragma unroll
   for (int cb = 0; cb < kCB; ++cb) acc[cb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  {
+  for (int i = 0; i < tpw; ++i) {
+    const int n = tile0 + i * kDecWaves + wave;
+    if (n >= nKBb) break;
+    asm volatile("" ::: "memory");   // keep the LDS operand reads inside the loop
+    const bool int8 = route_of(n);
+    const size_t si = ((size_t)b * a.nKB + n) * a.Hk + hk;
+    const uint16_t dk_bits = a.dK[si], dv_bits = a.dV[si];
+    uint4 kr[4][kS16];
+    {
+      const char* kbytes = int8 ? reinterpret_cast<const char*>(a.K8) : reinterpret_cast<const char*>(a.K);
+      const size_t row_bytes = int8 ? D : 2 * D;
+      // K8 and FP16 key rows differ only in their row length (D or 2 D bytes): lane lq reads
+      // bytes 16 * lq + 64 * s of the row for product s of a 16-key block.
+      const int kbase = n * kBlockN + 16 * (l16 >> 2) + (l16 & 3);
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) {
+        const int key = min(kbase + 4 * blk, Lkb - 1);   // keys past the length are masked below
+        const char* kp = kbytes + (((size_t)b * a.Lk + key) * a.Hk + hk) * row_bytes + 16 * lq;
+#pragma unroll
+        for (int s = 0; s < kS8; ++s) kr[blk][s] = ld_global_16(kp + 64 * s);
+        if (!int8) {
+#pragma unroll
+          for (int s = kS8; s < kS16; ++s) kr[blk][s] = ld_global_16(kp + 64 * s);
+        }
+      }
+    }
+    uint4 vr[kCB];
+    {
+      const int8_t* vt = a.V8 + ((((size_t)b * a.Hk + hk) * a.nKB + n) * D + l16) * kBlockN + 16 * lq;
+#pragma unroll
+      for (int cb = 0; cb < kCB; ++cb) vr[cb] = ld_global_16(vt + cb * 16 * kBlockN);
+    }
+    float sc[4][4];
+    if (int8) {
+      i32x4 c[4];
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) c[blk] = i32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int s = 0; s < kS8; ++s) {   // one query operand slice live at a time
+        const i32x4 qb = *reinterpret_cast<const i32x4*>(&q8[l16][64 * s + 16 * lq]);
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk)
+          c[blk] = __builtin_amdgcn_mfma_i32_16x16x64_i8(as_i32x4(kr[blk][s]), qb, c[blk], 0, 0, 0);
+      }
+      const float f = cq[l16] * half_bits_to_float(dk_bits);
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sc[blk][r] = (float)c[blk][r] * f;
+    } else {
+      f32x4 c[4];
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) c[blk] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int s = 0; s < kS16; ++s) {
+        const half8 qb = *reinterpret_cast<const half8*>(&q16[l16][32 * s + 8 * lq]);
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk)
+          c[blk] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(kr[blk][s]), qb, c[blk], 0, 0, 0);
+      }
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sc[blk][r] = c[blk][r] * a.scale_log2e;
+    }
+    const float dv = half_bits_to_float(dv_bits);
+    float mt = ninf;
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool ok = head_ok && n * kBlockN + 16 * lq + 4 * blk + r < Lkb;
+        sc[blk][r] = ok ? sc[blk][r] : ninf;
+        mt = fmaxf(mt, sc[blk][r]);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, kWave));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, kWave));
+    const float m_new = fmaxf(m_w, mt);
+    const float alpha = m_w == ninf ? 0.0f : __builtin_amdgcn_exp2f(m_w - m_new);
+    z_w *= alpha;
+#pragma unroll
+    for (int cb = 0; cb < kCB; ++cb) acc[cb] *= alpha;
+    m_w = m_new;
+    half8 pb[2];
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = sc[blk][r] == ninf ? 0.0f : __builtin_amdgcn_exp2f(sc[blk][r] - m_new);
+        z_w += p;
+        pb[blk >> 1][4 * (blk & 1) + r] = (_Float16)(p * dv);
+      }
 #pragma unroll
     for (int cb = 0; cb < kCB; ++cb) {
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(i8x8_to_half8(vr[cb].x, vr[cb].y), pb[0],
-                                                      acc[cb], 0, 0, 0);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(i8x8_to_half8(vr[cb].z, vr[cb].w), pb[1],
-                                                      acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(i8x8_to_half8(vr[cb].x, vr[cb].y), pb[0], acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(i8x8_to_half8(vr[cb].z, vr[cb].w), pb[1], acc[cb], 0, 0, 0);
     }
   }
+  // 4. Merge of the eight waves (log-sum-exp rule through LDS), then (max, normalizer,
+  //    unnormalized output) of the chunk per head.
+  z_w += __shfl_xor(z_w, 16, kWave);
+  z_w += __shfl_xor(z_w, 32, kWave);
+  if (lq == 0) red_m[wave][l16] = m_w;
+  __syncthreads();
+  float mc = red_m[0][l16];
+#pragma unroll
+  for (int w = 1; w < kDecWaves; ++w) mc = fmaxf(mc, red_m[w][l16]);
+  const float fw = m_w == ninf ? 0.0f : __builtin_amdgcn_exp2f(m_w - mc);
+  if (lq == 0) red_z[wave][l16] = z_w * fw;
   if (head_ok) {
 #pragma unroll
     for (int cb = 0; cb < kCB; ++cb)
-      *reinterpret_cast<f32x4*>(&osum[wave][l16][16 * cb + 4 * lq]) = acc[cb];
+      *reinterpret_cast<f32x4*>(&osum[wave][l16][16 * cb + 4 * lq]) = acc[cb] * fw;
   }
   __syncthreads();
-
-  // 7. Sum of the eight waves: (max, normalizer, unnormalized output) of the chunk per head.
   for (int o = tid; o < G * D; o += kDecThreads) {
     const int g = o / D, c = o % D;
     float sum = 0.0f;
@@ -289,7 +299,8 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeA
   int chunks = a.chunks;       // the chunks that hold keys of this sequence
   if (a.seqlens) {
     const int len = min(max(a.seqlens[bh / a.Hq], 0), a.Lk);
-    chunks = min(chunks, (len + kDecChunk - 1) / kDecChunk);
+    const int per = kDecWaves * a.tiles_per_wave;   // key tiles per chunk
+    chunks = min(chunks, ((len + kBlockN - 1) / kBlockN + per - 1) / per);
   }
   __shared__ float sm[kRows], sz[kRows];
   __shared__ f32x4 so[kRows][kLanes];
@@ -368,6 +379,17 @@ hipError_t launch_decode(const DecodeArgs& a, int d, hipStream_t stream) {
   return hipErrorInvalidValue;
 }
 
-int decode_chunks(int len_k) { return (len_k + kDecChunk - 1) / kDecChunk; }
+// Tiles each wave streams: the grid then holds about kDecSlots workgroups, one round on the
+// chip, however long the cache.
+int decode_tiles_per_wave(int batch, int heads_kv, int len_k) {
+  const long long tiles = (long long)batch * heads_kv * ((len_k + kBlockN - 1) / kBlockN);
+  const long long per = (long long)kDecWaves * kDecSlots;
+  return (int)std::max<long long>(1, (tiles + per - 1) / per);
+}
+
+int decode_chunks(int batch, int heads_kv, int len_k) {
+  const int per = kDecWaves * decode_tiles_per_wave(batch, heads_kv, len_k);
+  return ((len_k + kBlockN - 1) / kBlockN + per - 1) / per;
+}
 
 }  // namespace tilemix

@@ -470,7 +470,7 @@ tilemix_status check_decode(const tilemix_params* p) {
 }
 
 size_t decode_workspace(const tilemix_params* p) {
-  const size_t rows = (size_t)p->batch * p->heads_q * tilemix::decode_chunks(p->len_k);
+  const size_t rows = (size_t)p->batch * p->heads_q * tilemix::decode_chunks(p->batch, p->heads_kv, p->len_k);
   return align256(rows * sizeof(float)) * 2 + align256(rows * p->head_dim * sizeof(float));
 }
 
@@ -535,7 +535,8 @@ tilemix_status decode_impl(const tilemix_params* params, const int32_t* seqlens_
   a.O = static_cast<_Float16*>(O);
   a.B = p.batch; a.Hq = p.heads_q; a.Hk = p.heads_kv; a.Lk = p.len_k;
   a.W = (int)pl.W; a.g = p.group_size; a.nKB = (int)pl.nKB;
-  a.chunks = tilemix::decode_chunks(p.len_k);
+  a.chunks = tilemix::decode_chunks(p.batch, p.heads_kv, p.len_k);
+  a.tiles_per_wave = tilemix::decode_tiles_per_wave(p.batch, p.heads_kv, p.len_k);
   a.route_per_batch = p.route_per_batch;
   a.force_fp16 = p.route_hint == 0 ? 1 : 0;
   a.scale_log2e = p.scale * 1.4426950408889634f;

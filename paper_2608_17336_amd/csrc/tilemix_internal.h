@@ -81,6 +81,7 @@ struct DecodeArgs {
   // Sequence b uses its first min(max(seqlens[b], 0), Lk) cached keys; Lk is the capacity.
   const int* seqlens;
   int B, Hq, Hk, Lk, W, g, nKB, chunks;
+  int tiles_per_wave;      // key tiles each wave of the partial kernel streams
   int route_per_batch, force_fp16;
   float scale_log2e;
 };
@@ -107,7 +108,8 @@ hipError_t launch_seq_table(const int* cu_q, const int* cu_k, int batch, int tot
                             hipStream_t stream);
 hipError_t launch_routed_attention(const AttnArgs& args, int d, int block_m, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& args, int d, hipStream_t stream);
-int decode_chunks(int len_k);
+int decode_tiles_per_wave(int batch, int heads_kv, int len_k);
+int decode_chunks(int batch, int heads_kv, int len_k);
 hipError_t launch_debug_tiles(const DebugTileArgs& args, int d, int block_m, hipStream_t stream);
 
 }  // namespace tilemix

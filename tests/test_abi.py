@@ -129,7 +129,8 @@ def test_decode_rejects_before_launch():
     assert call(_cp(**dp), ptr=None) == 1
     assert call(_cp(**dp), ptr=ctypes.c_void_p(0x1001)) == 4
     assert call(_cp(**dp), ws=ctypes.c_void_p(0x100080)) == 4
-    # partial results: B * H_q * ceil(L_k / 512) chunks of (max, normalizer, d floats)
+    # partial results: B * H_q * ceil(L_k / 512) chunks of (max, normalizer, d floats) while the
+    # batch holds at most 2048 key tiles (one tile per wave of each 8-wave workgroup)
     need = tm.tilemix_decode_workspace_size(_cp(**dp))
     assert need >= 64 * 10 * (2 + 128) * 4
     assert call(_cp(**dp), ws=ok, ws_bytes=need - 1) == 5

@@ -112,8 +112,9 @@ def test_decode_full_workload_sampled():
 
 @pytest.mark.timeout(300)
 def test_decode_longest_cache_full_group():
-    """L_k = 262144 (the longest cache the build supports: 512 chunks to merge) with a
-    16-head GQA group (every matrix-core column used), g = 16 (four routing words)."""
+    """L_k = 262144 (the longest cache the build supports: each wave streams two tiles, 256
+    chunks to merge) with a 16-head GQA group (every matrix-core column used), g = 16 (four
+    routing words)."""
     import torch
     import paper_2608_17336_amd as tm
     Lk, g = 262144, 16
@@ -141,6 +142,8 @@ RAGGED = [
     (4, 8, 2, 128, 700, 2, [700, 1, 0, 333]),
     (3, 16, 1, 128, 5000, 4, [4999, 512, 513]),
     (2, 4, 4, 64, 300, 1, [64, 299]),
+    # 10016 key tiles in the batch: each wave streams 5 tiles, a chunk holds 40
+    (4, 32, 8, 128, 20000, 4, [20000, 1, 0, 7777]),
 ]
 
 
