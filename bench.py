@@ -420,8 +420,9 @@ def bench_decode(args, cfg, mask):
 
 def bench_varlen(args, cfg, mask):
     """One step = tilemix_prefill_varlen over a packed batch of the given sequence lengths
-    (sequence table, quantize-once, V tiles and the fused kernel), causal, with the workload's
-    heads, head size, tile, group size and routing mask kind drawn per sequence."""
+    (sequence table, key quantization, V tiles and the attention kernel), causal, with the
+    workload's heads, head size, tile, group size and routing mask kind drawn per sequence.
+    With --fused: tilemix_prefill_varlen_fused (no key quantization pass; codes made on chip)."""
     import numpy as np
     import torch
 
@@ -450,12 +451,13 @@ def bench_varlen(args, cfg, mask):
     w = to(np.concatenate(rows).view(np.int64))
     cu = to(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32))
     hint = 0 if mask.kind == "all_fp16" else -1
-    ws = torch.empty(tm.tilemix_varlen_workspace_size(p, sum(lens), sum(lens)), dtype=torch.uint8, device=dev)
+    size = tm.tilemix_varlen_fused_workspace_size if args.fused else tm.tilemix_varlen_workspace_size
+    ws = torch.empty(size(p, sum(lens), sum(lens)), dtype=torch.uint8, device=dev)
     O = torch.empty_like(q)
     stream = torch.cuda.current_stream()
-    run = lambda: tm.tilemix_prefill_varlen(q, k, v, cu, cu, Lmax, Lmax, w, cfg.group_size,
-                                            (cfg.block_m, cfg.block_n), True, cfg.scale, O=O,
-                                            workspace=ws, stream=stream, route_hint=hint)
+    entry = tm.tilemix_prefill_varlen_fused if args.fused else tm.tilemix_prefill_varlen
+    run = lambda: entry(q, k, v, cu, cu, Lmax, Lmax, w, cfg.group_size, (cfg.block_m, cfg.block_n),
+                        True, cfg.scale, O=O, workspace=ws, stream=stream, route_hint=hint)
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
@@ -479,7 +481,8 @@ def bench_varlen(args, cfg, mask):
         "data": "synthetic",
         "config": {"workload": f"varlen-{cfg.name}", "lens": lens, "Hq": cfg.Hq, "Hk": cfg.Hk,
                    "d": cfg.d, "tile": f"{cfg.block_m}x{cfg.block_n}", "group_size": cfg.group_size,
-                   "mask": mask.label, "rho_pairs": round(rho, 4)},
+                   "mask": mask.label, "rho_pairs": round(rho, 4),
+                   "operands": "fused on-the-fly" if args.fused else "quantize-once"},
         "step_ms_events": round(ms, 4),
         "pct_of_weighted_roofline": round(100.0 * t_star / (wall * 1e-3), 2),
         # one call enqueues the sequence table, the key quantization, the V tiles and the kernel,
@@ -487,8 +490,10 @@ def bench_varlen(args, cfg, mask):
         "roofline": {"bound": "mfma", "achieved": round(flops / (ms * 1e-3) / 1e12, 2),
                      "peak": round(flops / t_star / 1e12, 2), "unit": "TFLOP/s",
                      "frac": round(t_star / (ms * 1e-3), 4), "traffic": None,
-                     "kernel": f"tilemix_prefill_varlen (seq table, K quantization, V tiles, "
-                               f"routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1>)"},
+                     "kernel": (f"tilemix_prefill_varlen_fused (seq table, V tiles, "
+                                f"routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1, true>)" if args.fused else
+                                f"tilemix_prefill_varlen (seq table, K quantization, V tiles, "
+                                f"routed_attn_fwd_kernel<{cfg.d}, {cfg.block_m}, 1>)")},
     }
     print(json.dumps(line), flush=True)
     return 0

@@ -3,6 +3,7 @@ message (the benchmark measures one GPU), before anything touches a device."""
 
 import json
 import os
+import re
 import subprocess
 import sys
 
@@ -26,7 +27,8 @@ def test_recorded_traffic_needs_matching_mask_and_source():
     for profile, source in (("routed_attn_fwd_32k-gqa", "attn_fwd.hip"),
                             ("decode_64k-b4-gqa", "decode.hip")):
         path = os.path.join(ROOT, "profiles", f"{profile}_hbm_traffic.md")
-        fields = dict(line[2:].split(": ", 1) for line in open(path) if line.startswith("- "))
+        fields = dict(m.groups() for m in (re.match(r"^- (\w+): (`[^`]*`)$", line.strip())
+                                           for line in open(path)) if m)
         mask = fields["mask"].strip().strip("`")
         want = int(fields["traffic_bytes_per_launch"].strip().strip("`"))
         digest = fields["kernel_source_sha256"].strip().strip("`")
