@@ -304,7 +304,10 @@ tilemix_status tilemix_quantize_kv(const tilemix_params* params, const void* K, 
                                    int8_t* K8, uint16_t* dK, int8_t* V8, uint16_t* dV,
                                    void* stream);
 
-/* Bytes of device workspace tilemix_decode needs (per-chunk partial results), 256-aligned. */
+/* Bytes of device workspace tilemix_decode needs, 256-aligned: per (sequence, query head, chunk)
+ * the chunk's max, normalizer and d FP32 output values.  A chunk is 8 t key tiles of 64, with
+ * t = max(1, ceil(B H_k ceil(L_k/64) / 2048)) tiles per wave, so that the partial kernel runs
+ * about 256 workgroups (one per CU); the size depends only on params. */
 tilemix_status tilemix_decode_workspace_size(const tilemix_params* params, size_t* bytes);
 
 /*
