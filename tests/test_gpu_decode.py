@@ -37,6 +37,8 @@ CASES = [
     (1, 16, 1, 128, 700, 2, False),
     (3, 6, 2, 64, 300, 1, False),
     (1, 2, 1, 64, 257, 3, True),
+    # MHA (one head per group, 15 padding columns), 20032 key tiles: each wave streams 10 tiles
+    (8, 8, 8, 64, 20000, 2, False),
 ]
 
 
